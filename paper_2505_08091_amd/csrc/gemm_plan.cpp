@@ -1,0 +1,501 @@
+// GEMM planning.  See gemm_plan.hpp and kernels/gemm.hip.
+#include "gemm_plan.hpp"
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <sstream>
+#include <tuple>
+
+#include "errors.hpp"
+#include "lower.hpp"
+
+namespace lego {
+
+LayoutP mfma_fragment_layout(int instr, int operand) {
+  if (instr == 0) {
+    // v_mfma_f32_32x32x16: A/B lane l holds row (or column) l%32, k = 8*(l/32)+e;
+    // C/D register r of lane l is row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+    if (operand == 0 || operand == 1) return make_orderby(make_groupby({64, 8}), {make_regp({2, 32, 8}, {2, 1, 3})});
+    if (operand == 2) return make_orderby(make_groupby({64, 16}), {make_regp({2, 32, 4, 4}, {3, 1, 4, 2})});
+  } else if (instr == 1) {
+    // v_mfma_f32_16x16x32: A/B lane l holds row l%16, k = 8*(l/16)+e;
+    // C/D register r of lane l is row 4*(l/16) + r, column l%16.
+    if (operand == 0 || operand == 1) return make_orderby(make_groupby({64, 8}), {make_regp({4, 16, 8}, {2, 1, 3})});
+    if (operand == 2) return make_orderby(make_groupby({64, 4}), {make_regp({4, 16, 4}, {1, 3, 2})});
+  }
+  throw std::invalid_argument("unknown MFMA instruction or operand");
+}
+
+GemmRequest gemm_request(const lego_gemm_desc& d, const std::function<LayoutP(lego_layout_t)>& resolve) {
+  GemmRequest r;
+  r.M = d.M;
+  r.N = d.N;
+  r.K = d.K;
+  r.dtype = d.in_dtype;
+  r.bm = d.bm;
+  r.bn = d.bn;
+  r.bk = d.bk;
+  r.wm = d.wm;
+  r.wn = d.wn;
+  r.group_m = d.group_m;
+  r.xcd = d.xcd_remap;
+  r.a = resolve(d.a);
+  r.b = resolve(d.b);
+  r.c = resolve(d.c);
+  r.sched = resolve(d.sched);
+  r.lds_a = resolve(d.lds_a);
+  r.lds_b = resolve(d.lds_b);
+  return r;
+}
+
+namespace {
+
+bool pow2(i64 x) { return x > 0 && (x & (x - 1)) == 0; }
+
+LayoutP default_lds(i64 rows, i64 k) {
+  if (k % 8 == 0 && pow2(k / 8) && k / 8 >= 2) return make_from_piece(make_genp(GEN_XOR_SWIZZLE, {rows, k}, {8, 1}));
+  return make_from_piece(make_row({rows, k}));
+}
+
+void need_dims(const LayoutP& l, std::vector<i64> d, const char* what) {
+  if (l->dims() != d) throw std::length_error(std::string(what) + " layout has the wrong logical shape");
+  if (l->expand_inner) throw Unsupported(std::string(what) + ": ExpandBy layouts are not supported by the GEMM");
+}
+
+// Does `off` (a function of e and other variables) advance by exactly e, with
+// the e = 0 offset a multiple of v?
+bool contiguous_in(const Sum& off, int e, int v) {
+  Sum ep, rest;
+  std::vector<int> g = {e};
+  if (!split_by(off, g, &ep, &rest)) return false;
+  Ctx dummy;
+  if (ep.c0 != 0 || ep.t.size() != 1 || ep.t[0].c != 1) return false;
+  const Atom& a = *ep.t[0].a;
+  if (a.op != Op::Field || a.var != e || a.a != 1 || a.b != 0) return false;
+  if (rest.c0 % v) return false;
+  for (auto& t : rest.t)
+    if (t.c % v) return false;
+  return true;
+}
+
+struct Operand {
+  // tile [R, KD]: R along m (A) or n (B), KD along k
+  i64 R, KD;
+  LayoutP glob, lds;
+  bool is_b;
+  int V = 1, axis = 1, NV = 1;
+  i64 NVEC = 0;
+  bool guard = false, sep = false, svec = false, frvec = false;
+};
+
+}  // namespace
+
+GemmPlan plan_gemm(const GemmRequest& rq0) {
+  GemmRequest rq = rq0;
+  if (rq.dtype != LEGO_F16 && rq.dtype != LEGO_BF16) throw std::invalid_argument("GEMM inputs must be fp16 or bf16");
+  if (rq.M <= 0 || rq.N <= 0 || rq.K <= 0) throw std::invalid_argument("GEMM sizes must be positive");
+  if (!rq.bm) rq.bm = (int)std::min<i64>(256, rq.M);
+  if (!rq.bn) rq.bn = (int)std::min<i64>(256, rq.N);
+  if (!rq.bk) rq.bk = (int)std::min<i64>(64, rq.K);
+  if (!rq.wm) rq.wm = rq.bm >= 64 ? rq.bm / 2 : rq.bm;
+  if (!rq.wn) rq.wn = rq.bn >= 64 ? rq.bn / 2 : rq.bn;
+  if (!rq.group_m) rq.group_m = 8;
+  const i64 M = rq.M, N = rq.N, K = rq.K;
+  const int bm = rq.bm, bn = rq.bn, bk = rq.bk, wm = rq.wm, wn = rq.wn;
+  if (bm <= 0 || bn <= 0 || bk <= 0 || wm <= 0 || wn <= 0) throw std::invalid_argument("tile sizes must be positive");
+  if (M % bm || N % bn || K % bk) throw Unsupported("GEMM sizes must be multiples of the workgroup tile");
+  const int MB = (wm % 32 == 0 && wn % 32 == 0) ? 32 : 16;
+  const int KB = MB == 32 ? 16 : 32;
+  if (wm % MB || wn % MB || bm % wm || bn % wn || bk % KB)
+    throw Unsupported("wave tile must be a multiple of the MFMA block and divide the workgroup tile");
+  const int NWM = bm / wm, NWN = bn / wn, NWAVES = NWM * NWN, NT = 64 * NWAVES;
+  if (NT > 1024) throw Unsupported("more than 16 waves per workgroup");
+  const int MI = wm / MB, NI = wn / MB, NREG = MB == 32 ? 16 : 4;
+  if (MI * NI * NREG > 256) throw Unsupported("wave tile needs more than 256 accumulator registers");
+  const i64 lds_bytes = 2ll * (bm + bn) * bk * 2;
+  if (lds_bytes > 160 * 1024) throw Unsupported("two LDS stages exceed 160 KiB");
+  const i64 Mt = M / bm, Nt = N / bn, Kt = K / bk, P = Mt * Nt;
+
+  LayoutP LA = rq.a ? rq.a : make_from_piece(make_row({M, K}));
+  LayoutP LB = rq.b ? rq.b : make_from_piece(make_col({K, N}));
+  LayoutP LC = rq.c ? rq.c : make_from_piece(make_row({M, N}));
+  need_dims(LA, {M, K}, "A");
+  need_dims(LB, {K, N}, "B");
+  need_dims(LC, {M, N}, "C");
+  const i64 G = std::min<i64>(rq.group_m, Mt);
+  LayoutP SCH = rq.sched;
+  if (!SCH) {
+    if (Mt % G == 0 && G > 1)
+      SCH = make_orderby(make_groupby({Mt, Nt}), {make_regp({Mt / G, G, Nt}, {1, 3, 2})});
+    else
+      SCH = make_from_piece(make_row({Mt, Nt}));
+  }
+  need_dims(SCH, {Mt, Nt}, "schedule");
+  const bool xcd = rq.xcd && P % 8 == 0;
+  LayoutP XCD = xcd ? make_orderby(make_groupby({P / 8, 8}), {make_regp({P / 8, 8}, {2, 1})}) : nullptr;
+  LayoutP SA = rq.lds_a ? rq.lds_a : default_lds(bm, bk);
+  LayoutP SB = rq.lds_b ? rq.lds_b : default_lds(bn, bk);
+  need_dims(SA, {bm, bk}, "LDS A");
+  need_dims(SB, {bn, bk}, "LDS B");
+  LayoutP FA = mfma_fragment_layout(MB == 32 ? 0 : 1, 0);
+  LayoutP FC = mfma_fragment_layout(MB == 32 ? 0 : 1, 2);
+
+  Operand ops[2] = {{bm, bk, LA, SA, false}, {bn, bk, LB, SB, true}};
+  // With a single round of load vectors, only threads below NVEC load; giving
+  // tid that range lets the range analysis prove separability.
+  auto tid_ext = [&](const Operand& o) -> i64 { return o.NV == 1 ? std::min<i64>(NT, o.NVEC) : NT; };
+
+  // Global element offset of tile element (i, j) for tile coordinates (tt, kt).
+  auto glob_off = [&](Ctx& c, const Operand& o, const Sum& tt, const Sum& kt, const Sum& i, const Sum& j) {
+    SymAlg al{&c};
+    Sum row = add(c, mulc(c, tt, o.R), i);
+    Sum kk = add(c, mulc(c, kt, o.KD), j);
+    return o.is_b ? o.glob->apply(al, {kk, row}) : o.glob->apply(al, {row, kk});
+  };
+  // Tile element (i, j) of load vector u of thread tid, plus element e.
+  auto load_elem = [&](Ctx& c, const Operand& o, const Sum& tid, const Sum& u, const Sum& e, Sum* i, Sum* j) {
+    Sum q = add(c, mulc(c, u, NT), tid);
+    if (o.axis == 1) {
+      i64 per = o.KD / o.V;
+      *i = fdiv(c, q, per);
+      *j = add(c, mulc(c, fmod(c, q, per), o.V), e);
+    } else {
+      i64 per = o.R / o.V;
+      *i = add(c, mulc(c, fmod(c, q, per), o.V), e);
+      *j = fdiv(c, q, per);
+    }
+  };
+
+  for (Operand& o : ops) {
+    // Largest vector (16 bytes at most) along either tile axis that is
+    // contiguous and aligned in global memory.
+    o.V = 1;
+    o.axis = 1;
+    for (int v : {8, 4, 2}) {
+      bool found = false;
+      for (int axis : {1, 0}) {
+        i64 ext = axis == 1 ? o.KD : o.R;
+        if (ext % v) continue;
+        Ctx c;
+        int tt = c.var("tt", o.is_b ? Nt : Mt), kt = c.var("kt", Kt);
+        int x = c.var("x", ext / v), y = c.var("y", axis == 1 ? o.R : o.KD), e = c.var("e", v);
+        Sum xs = add(c, mulc(c, var(c, x), v), var(c, e));
+        Sum off = axis == 1 ? glob_off(c, o, var(c, tt), var(c, kt), var(c, y), xs)
+                            : glob_off(c, o, var(c, tt), var(c, kt), xs, var(c, y));
+        if (contiguous_in(off, e, v)) {
+          o.V = v;
+          o.axis = axis;
+          found = true;
+          break;
+        }
+      }
+      if (found) break;
+    }
+    o.NVEC = o.R * o.KD / o.V;
+    o.NV = (int)((o.NVEC + NT - 1) / NT);
+    o.guard = o.NVEC % NT != 0;
+    // Additive separability of the global offset into tile, k-step and thread parts.
+    {
+      Ctx c;
+      int tt = c.var("tt", o.is_b ? Nt : Mt), kt = c.var("kt", Kt), tid = c.var("tid", tid_ext(o)),
+          u = c.var("u", o.NV);
+      Sum i, j;
+      load_elem(c, o, var(c, tid), var(c, u), cst(0), &i, &j);
+      Sum off = glob_off(c, o, var(c, tt), var(c, kt), i, j);
+      Sum pt, r1, pk, pl;
+      o.sep = split_by(off, {tt}, &pt, &r1) && split_by(r1, {kt}, &pk, &pl);
+    }
+    // Vector LDS store?
+    {
+      Ctx c;
+      int tid = c.var("tid", tid_ext(o)), u = c.var("u", o.NV), e = c.var("e", o.V);
+      Sum i, j;
+      load_elem(c, o, var(c, tid), var(c, u), var(c, e), &i, &j);
+      SymAlg al{&c};
+      o.svec = o.V > 1 && contiguous_in(o.lds->apply(al, {i, j}), e, o.V);
+      if (o.V == 1) o.svec = true;
+    }
+    // Vector fragment read?
+    {
+      Ctx c;
+      int lane = c.var("lane", 64), w = c.var("w", NWAVES), mi = c.var("mi", o.is_b ? NI : MI),
+          s = c.var("s", bk / KB), e = c.var("e", 8);
+      SymAlg al{&c};
+      Sum f = FA->apply(al, {var(c, lane), var(c, e)});
+      Sum r = fdiv(c, f, KB), k = fmod(c, f, KB);
+      Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+      Sum kk = add(c, mulc(c, var(c, s), KB), k);
+      o.frvec = contiguous_in(o.lds->apply(al, {row, kk}), e, 8);
+    }
+  }
+
+  // ----- emit the index functions
+  using Builder = std::function<FnSpec(Ctx&)>;
+  std::vector<std::pair<std::string, Builder>> fns;
+  // Parts of one additive split (a_gt/a_gk/a_gl, b_*, c_t/c_l) are all taken
+  // from the expanded lowering, the one the separability check used.
+  auto is_part = [](const std::string& n) {
+    return n == "a_gt" || n == "a_gk" || n == "a_gl" || n == "b_gt" || n == "b_gk" || n == "b_gl" || n == "c_t" ||
+           n == "c_l";
+  };
+  fns.push_back({"sched", [&](Ctx& c) {
+                   SymAlg al{&c};
+                   int pid = c.var("pid", P);
+                   Sum q = var(c, pid);
+                   if (xcd) q = XCD->apply(al, unflatten(al, {P / 8, 8}, q));
+                   FnSpec f;
+                   f.params = {pid};
+                   f.outs = SCH->inv(al, q);
+                   return f;
+                 }});
+  const char* pre[2] = {"a_", "b_"};
+  for (int k = 0; k < 2; ++k) {
+    const Operand& o = ops[k];
+    std::string p = pre[k];
+    auto full = [&, k](Ctx& c, int* tt, int* kt, int* tid, int* u) {
+      const Operand& oo = ops[k];
+      *tt = c.var(oo.is_b ? "tn" : "tm", oo.is_b ? Nt : Mt);
+      *kt = c.var("kt", Kt);
+      *tid = c.var("tid", tid_ext(oo));
+      *u = c.var("u", oo.NV);
+      Sum i, j;
+      load_elem(c, oo, var(c, *tid), var(c, *u), cst(0), &i, &j);
+      return glob_off(c, oo, var(c, *tt), var(c, *kt), i, j);
+    };
+    if (o.sep) {
+      fns.push_back({p + "gt", [=](Ctx& c) {
+                       int tt, kt, tid, u;
+                       Sum off = full(c, &tt, &kt, &tid, &u), a, r;
+                       FnSpec f;
+                       f.valid = split_by(off, {tt}, &a, &r);
+                       f.params = {tt};
+                       f.outs = {a};
+                       return f;
+                     }});
+      fns.push_back({p + "gk", [=](Ctx& c) {
+                       int tt, kt, tid, u;
+                       Sum off = full(c, &tt, &kt, &tid, &u), a, r, kp, l;
+                       FnSpec f;
+                       f.valid = split_by(off, {tt}, &a, &r) && split_by(r, {kt}, &kp, &l);
+                       f.params = {kt};
+                       f.outs = {kp};
+                       return f;
+                     }});
+      fns.push_back({p + "gl", [=](Ctx& c) {
+                       int tt, kt, tid, u;
+                       Sum off = full(c, &tt, &kt, &tid, &u), a, r, kp, l;
+                       FnSpec f;
+                       f.valid = split_by(off, {tt}, &a, &r) && split_by(r, {kt}, &kp, &l);
+                       f.params = {tid, u};
+                       f.outs = {l};
+                       return f;
+                     }});
+    } else {
+      fns.push_back({p + "gf", [=](Ctx& c) {
+                       int tt, kt, tid, u;
+                       Sum off = full(c, &tt, &kt, &tid, &u);
+                       FnSpec f;
+                       f.params = {tt, kt, tid, u};
+                       f.outs = {off};
+                       return f;
+                     }});
+    }
+    fns.push_back({p + "s", [&, k](Ctx& c) {
+                     const Operand& oo = ops[k];
+                     int tid = c.var("tid", tid_ext(oo)), u = c.var("u", oo.NV), e = c.var("e", oo.V);
+                     Sum i, j;
+                     load_elem(c, oo, var(c, tid), var(c, u), var(c, e), &i, &j);
+                     SymAlg al{&c};
+                     FnSpec f;
+                     f.params = {tid, u, e};
+                     f.outs = {oo.lds->apply(al, {i, j})};
+                     return f;
+                   }});
+    fns.push_back({p + "fr", [&, k](Ctx& c) {
+                     const Operand& oo = ops[k];
+                     int lane = c.var("lane", 64), w = c.var("w", NWAVES), mi = c.var("mi", oo.is_b ? NI : MI),
+                         s = c.var("s", bk / KB), e = c.var("e", 8);
+                     SymAlg al{&c};
+                     Sum f0 = FA->apply(al, {var(c, lane), var(c, e)});
+                     Sum r = fdiv(c, f0, KB), kq = fmod(c, f0, KB);
+                     Sum wpos = oo.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+                     Sum row = add(c, add(c, mulc(c, wpos, oo.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+                     Sum kk = add(c, mulc(c, var(c, s), KB), kq);
+                     FnSpec f;
+                     f.params = {lane, w, mi, s, e};
+                     f.outs = {oo.lds->apply(al, {row, kk})};
+                     return f;
+                   }});
+  }
+  auto c_full = [&](Ctx& c, int* tm, int* tn, int* lane, int* w, int* mi, int* ni, int* r) {
+    *tm = c.var("tm", Mt);
+    *tn = c.var("tn", Nt);
+    *lane = c.var("lane", 64);
+    *w = c.var("w", NWAVES);
+    *mi = c.var("mi", MI);
+    *ni = c.var("ni", NI);
+    *r = c.var("r", NREG);
+    SymAlg al{&c};
+    Sum f0 = FC->apply(al, {var(c, *lane), var(c, *r)});
+    Sum row = fdiv(c, f0, MB), col = fmod(c, f0, MB);
+    Sum m = add(c, add(c, mulc(c, var(c, *tm), bm), mulc(c, fdiv(c, var(c, *w), NWN), wm)),
+                add(c, mulc(c, var(c, *mi), MB), row));
+    Sum n = add(c, add(c, mulc(c, var(c, *tn), bn), mulc(c, fmod(c, var(c, *w), NWN), wn)),
+                add(c, mulc(c, var(c, *ni), MB), col));
+    return LC->apply(al, {m, n});
+  };
+  bool csep = false;
+  {
+    Ctx c;
+    int tm, tn, lane, w, mi, ni, r;
+    Sum off = c_full(c, &tm, &tn, &lane, &w, &mi, &ni, &r), a, b;
+    csep = split_by(off, {tm, tn}, &a, &b);
+  }
+  if (csep) {
+    fns.push_back({"c_t", [&](Ctx& c) {
+                     int tm, tn, lane, w, mi, ni, r;
+                     Sum off = c_full(c, &tm, &tn, &lane, &w, &mi, &ni, &r), a, b;
+                     FnSpec f;
+                     f.valid = split_by(off, {tm, tn}, &a, &b);
+                     f.params = {tm, tn};
+                     f.outs = {a};
+                     return f;
+                   }});
+    fns.push_back({"c_l", [&](Ctx& c) {
+                     int tm, tn, lane, w, mi, ni, r;
+                     Sum off = c_full(c, &tm, &tn, &lane, &w, &mi, &ni, &r), a, b;
+                     FnSpec f;
+                     f.valid = split_by(off, {tm, tn}, &a, &b);
+                     f.params = {lane, w, mi, ni, r};
+                     f.outs = {b};
+                     return f;
+                   }});
+  } else {
+    fns.push_back({"c_f", [&](Ctx& c) {
+                     int tm, tn, lane, w, mi, ni, r;
+                     Sum off = c_full(c, &tm, &tn, &lane, &w, &mi, &ni, &r);
+                     FnSpec f;
+                     f.params = {tm, tn, lane, w, mi, ni, r};
+                     f.outs = {off};
+                     return f;
+                   }});
+  }
+
+  bool wide = false;
+  for (auto& f : fns) wide = wide || emit_best(f.first, f.second, false, is_part(f.first) ? 0 : -1).wide;
+  std::string code;
+  std::ostringstream opsinfo;
+  for (auto& f : fns) {
+    Emitted e = emit_best(f.first, f.second, wide, is_part(f.first) ? 0 : -1);
+    code += e.code;
+    opsinfo << " " << f.first << ":" << e.ops;
+  }
+
+  std::ostringstream s;
+  s << prelude_text() << "#define IDX_T " << (wide ? "i64" : "u32") << "\n"
+    << "#define BM " << bm << "\n#define BN " << bn << "\n#define BK " << bk << "\n#define MB " << MB
+    << "\n#define KB " << KB << "\n#define MI " << MI << "\n#define NI " << NI << "\n#define NWAVES " << NWAVES
+    << "\n#define NT " << NT << "\n#define KT " << Kt << "u\n#define IN_BF16 " << (rq.dtype == LEGO_BF16 ? 1 : 0)
+    << "\n#define GEMM_M " << M << "ull\n#define GEMM_N " << N << "ull\n#define GEMM_K " << K << "ull\n#define GEMM_MT "
+    << Mt << "ull\n#define GEMM_NT " << Nt << "ull\n";
+  const char* P2[2] = {"A_", "B_"};
+  for (int k = 0; k < 2; ++k) {
+    const Operand& o = ops[k];
+    s << "#define " << P2[k] << "NV " << o.NV << "\n#define " << P2[k] << "V " << o.V << "\n#define " << P2[k]
+      << "SEP " << (o.sep ? 1 : 0) << "\n#define " << P2[k] << "SVEC " << (o.svec ? 1 : 0) << "\n#define " << P2[k]
+      << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "NVEC " << o.NVEC << "u\n#define " << P2[k]
+      << "GUARD " << (o.guard ? 1 : 0) << "\n";
+  }
+  s << "#define C_SEP " << (csep ? 1 : 0) << "\n" << code << "// ---- template ----\n" << tpl_gemm;
+
+  GemmPlan g;
+  g.src = s.str();
+  g.kernel = "lego_gemm";
+  g.grid = P;
+  g.block = NT;
+  std::ostringstream info;
+  info << "gemm " << M << "x" << N << "x" << K << (rq.dtype == LEGO_BF16 ? " bf16" : " f16") << " tile " << bm << "x"
+       << bn << "x" << bk << " waves " << NWM << "x" << NWN << " wave " << wm << "x" << wn << " mfma " << MB << "x"
+       << MB << "x" << KB << " sched" << (xcd ? "+xcd" : "") << " A:V" << ops[0].V << (ops[0].axis ? "k" : "m")
+       << (ops[0].sep ? " sep" : " full") << (ops[0].svec ? " svec" : " sscalar")
+       << (ops[0].frvec ? " frvec" : " frscalar") << " B:V" << ops[1].V << (ops[1].axis ? "k" : "n")
+       << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
+       << (ops[1].frvec ? " frvec" : " frscalar") << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
+       << " lds " << lds_bytes << "B ops" << opsinfo.str();
+  g.info = info.str();
+  return g;
+}
+
+namespace {
+std::mutex g_mu;
+std::map<std::string, std::pair<std::vector<LayoutP>, std::shared_ptr<GemmPlan>>> g_cache;
+}  // namespace
+
+std::shared_ptr<GemmPlan> gemm_plan_cached(const GemmRequest& rq) {
+  std::ostringstream k;
+  k << rq.M << "," << rq.N << "," << rq.K << "," << rq.dtype << "," << rq.bm << "," << rq.bn << "," << rq.bk << ","
+    << rq.wm << "," << rq.wn << "," << rq.group_m << "," << rq.xcd;
+  for (auto* l : {&rq.a, &rq.b, &rq.c, &rq.sched, &rq.lds_a, &rq.lds_b}) k << "," << (const void*)l->get();
+  std::string key = k.str();
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) return it->second.second;
+  }
+  auto p = std::make_shared<GemmPlan>(plan_gemm(rq));
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_cache[key] = {{rq.a, rq.b, rq.c, rq.sched, rq.lds_a, rq.lds_b}, p};
+  return p;
+}
+
+std::vector<std::pair<std::string, std::string>> selftest_sources() {
+  std::vector<std::pair<std::string, std::string>> out;
+  // Index maps of the 128 x 128 three-level tiled layout.
+  LayoutP c1 = make_tileorderby({make_row({2, 2}), make_row({4, 4}), make_row({16, 16})});
+  out.push_back({"index apply 128x128 tiled", plan_index_eval(*c1, 0, 4).src});
+  out.push_back({"index inv 128x128 tiled", plan_index_eval(*c1, 1, 4).src});
+  // Row <-> blocked remap of 8192^2 fp32.
+  LayoutP row = make_from_piece(make_row({8192, 8192}));
+  LayoutP blk = make_tileorderby({make_col({128, 128}), make_row({64, 64})});
+  out.push_back({"remap row->blocked f32", plan_remap(*row, *blk, 4).src});
+  out.push_back({"remap blocked->row f32", plan_remap(*blk, *row, 4).src});
+  // Row <-> Morton remap of 4096^2 fp16, and the transpose.
+  LayoutP r4 = make_from_piece(make_row({4096, 4096}));
+  LayoutP mz = make_from_piece(make_genp(GEN_MORTON, {4096, 4096}, {}));
+  out.push_back({"remap row->morton f16", plan_remap(*r4, *mz, 2).src});
+  out.push_back({"remap morton->row f16", plan_remap(*mz, *r4, 2).src});
+  LayoutP col = make_from_piece(make_col({8192, 8192}));
+  out.push_back({"remap row->col f32", plan_remap(*row, *col, 4).src});
+  // GEMMs.
+  GemmRequest g1;
+  g1.M = g1.N = g1.K = 128;
+  g1.dtype = LEGO_F16;
+  g1.bm = g1.bn = 64;
+  g1.bk = 32;
+  g1.wm = g1.wn = 16;
+  out.push_back({"gemm 128^3 f16 64x64x32 wave 16x16", plan_gemm(g1).src});
+  GemmRequest g3;
+  g3.M = g3.N = g3.K = 1024;
+  g3.dtype = LEGO_F16;
+  g3.bm = g3.bn = 128;
+  g3.bk = 32;
+  g3.wm = g3.wn = 64;
+  out.push_back({"gemm 1024^3 f16 128x128x32", plan_gemm(g3).src});
+  GemmRequest g4;
+  g4.M = g4.N = g4.K = 8192;
+  g4.dtype = LEGO_BF16;
+  g4.xcd = 1;
+  out.push_back({"gemm 8192^3 bf16 256x256x64", plan_gemm(g4).src});
+  GemmRequest g5;
+  g5.M = g5.N = g5.K = 4096;
+  g5.dtype = LEGO_F16;
+  g5.a = mz;
+  g5.b = r4;
+  g5.xcd = 1;
+  out.push_back({"gemm 4096^3 f16 morton A, row B", plan_gemm(g5).src});
+  return out;
+}
+
+}  // namespace lego

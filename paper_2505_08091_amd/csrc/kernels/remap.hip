@@ -1,0 +1,77 @@
+// Layout remap kernels: dst[p] = src[M(p)] with M = L_src.apply o L_dst.inv.
+// Generated code defines, before this text:
+//   ELEM_T     unsigned integer type of the element size (bytes are copied)
+//   IDX_T      index type of the generated functions
+// Direct path (M keeps runs of at least V elements):
+//   V, NVEC, NT, UNROLL
+//   LEGO_FN IDX_T src_vec(IDX_T t)   source vector index of destination vector t
+// LDS path (both sides are digit permutations; a tile of TILE elements is read
+// in source order into LDS and written in destination order):
+//   TILE, NT, VL, VS, LDSW_CONTIG
+//   LEGO_FN IDX_T src_off(IDX_T g, IDX_T q)   element offset of source-side vector q of tile g
+//   LEGO_FN IDX_T ldsw(IDX_T q, IDX_T e)      LDS slot of element e of that vector
+//   LEGO_FN IDX_T ldsr(IDX_T q)               LDS slot of destination-side vector q
+//   LEGO_FN IDX_T dst_off(IDX_T g, IDX_T q)   element offset of destination-side vector q
+// NONTEMPORAL selects streaming (non-temporal) global loads and stores.
+
+#if NONTEMPORAL
+#define LEGO_LD(p) __builtin_nontemporal_load(p)
+#define LEGO_ST(v, p) __builtin_nontemporal_store((v), (p))
+#else
+#define LEGO_LD(p) (*(p))
+#define LEGO_ST(v, p) (*(p) = (v))
+#endif
+
+#ifdef LEGO_REMAP_DIRECT
+typedef ELEM_T vec_t __attribute__((ext_vector_type(V)));
+extern "C" __global__ __launch_bounds__(NT) void lego_remap_direct(const vec_t* __restrict__ src,
+                                                                   vec_t* __restrict__ dst) {
+  const u64 base = (u64)blockIdx.x * (NT * UNROLL) + threadIdx.x;
+  vec_t v[UNROLL];
+#pragma unroll
+  for (int u = 0; u < UNROLL; ++u) {
+    const u64 t = base + (u64)u * NT;
+    if (t < NVEC) v[u] = LEGO_LD(src + src_vec((IDX_T)t));
+  }
+#pragma unroll
+  for (int u = 0; u < UNROLL; ++u) {
+    const u64 t = base + (u64)u * NT;
+    if (t < NVEC) LEGO_ST(v[u], dst + t);
+  }
+}
+#endif
+
+#ifdef LEGO_REMAP_LDS
+typedef ELEM_T vl_t __attribute__((ext_vector_type(VL)));
+typedef ELEM_T vs_t __attribute__((ext_vector_type(VS)));
+extern "C" __global__ __launch_bounds__(NT) void lego_remap_lds(const ELEM_T* __restrict__ src,
+                                                                ELEM_T* __restrict__ dst) {
+  __shared__ ELEM_T tile[TILE];
+  const IDX_T g = blockIdx.x;
+  // Source-order phase: coalesced vector reads, scattered LDS writes.
+  vl_t v[TILE / VL / NT];
+#pragma unroll
+  for (int it = 0; it < TILE / VL / NT; ++it) {
+    const IDX_T q = it * NT + threadIdx.x;
+    v[it] = LEGO_LD((const vl_t*)(src + src_off(g, q)));
+  }
+#pragma unroll
+  for (int it = 0; it < TILE / VL / NT; ++it) {
+    const IDX_T q = it * NT + threadIdx.x;
+#if LDSW_CONTIG
+    *(vl_t*)&tile[ldsw(q, 0)] = v[it];
+#else
+#pragma unroll
+    for (int e = 0; e < VL; ++e) tile[ldsw(q, e)] = v[it][e];
+#endif
+  }
+  __syncthreads();
+  // Destination-order phase: vector LDS reads, coalesced vector writes.
+#pragma unroll
+  for (int it = 0; it < TILE / VS / NT; ++it) {
+    const IDX_T q = it * NT + threadIdx.x;
+    const vs_t w = *(const vs_t*)&tile[ldsr(q)];
+    LEGO_ST(w, (vs_t*)(dst + dst_off(g, q)));
+  }
+}
+#endif

@@ -1,0 +1,42 @@
+// Kernel planning: from layouts to a generated source, a kernel name and a
+// launch shape.  Planning needs no GPU (the build check compiles every plan's
+// source for gfx950); launching does.
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "layout.hpp"
+
+namespace lego {
+
+struct KernelPlan {
+  std::string src;      // complete generated HIP source
+  std::string kernel;   // extern "C" kernel name
+  long long grid = 1;   // workgroups (1D)
+  int block = 256;      // threads per workgroup
+  std::string info;     // human-readable summary (path, vector widths, op counts)
+};
+
+// Index-map evaluation over all points: which = 0 apply (logical flat order),
+// which = 1 inv (physical order, `rank` outputs per point).
+KernelPlan plan_index_eval(const Layout& l, int which, int idx_bytes);
+
+enum RemapPath { REMAP_DIRECT = 0, REMAP_LDS = 1, REMAP_GATHER = 2 };
+
+struct RemapPlan : KernelPlan {
+  int path = REMAP_GATHER;
+  long long run = 1;    // contiguous run of M (elements)
+  int vec = 1;          // elements per vector (direct) or source-side vector (LDS)
+  int vec_dst = 1;      // destination-side vector (LDS)
+  long long tile = 0;   // elements per LDS tile
+};
+
+RemapPlan plan_remap(const Layout& src, const Layout& dst, int elem_bytes);
+
+// Template texts, embedded at build time from csrc/kernels/*.hip.
+extern const char* const tpl_index_eval;
+extern const char* const tpl_remap;
+extern const char* const tpl_gemm;
+
+}  // namespace lego

@@ -1,0 +1,394 @@
+// Planning of index-map evaluation and layout remap kernels.
+#include <algorithm>
+#include <sstream>
+#include <stdexcept>
+
+#include "errors.hpp"
+#include "lower.hpp"
+#include "plans.hpp"
+
+namespace lego {
+
+namespace {
+
+const char* elem_type(int bytes) {
+  switch (bytes) {
+    case 1: return "unsigned char";
+    case 2: return "unsigned short";
+    case 4: return "unsigned int";
+    case 8: return "unsigned long long";
+  }
+  throw std::invalid_argument("element size must be 1, 2, 4 or 8 bytes");
+}
+
+std::string header() { return std::string(prelude_text()); }
+
+// Emit every function with one common index type (64-bit if any needs it).
+std::string emit_all(std::vector<std::pair<std::string, std::function<FnSpec(Ctx&)>>> fns, bool* wide_out,
+                     std::string* info) {
+  bool wide = false;
+  for (auto& f : fns) wide = wide || emit_best(f.first, f.second).wide;
+  std::string code;
+  for (auto& f : fns) {
+    Emitted e = emit_best(f.first, f.second, wide);
+    code += e.code;
+    if (info) *info += " " + f.first + ":" + std::to_string(e.ops) + "ops";
+  }
+  *wide_out = wide;
+  return code;
+}
+
+}  // namespace
+
+KernelPlan plan_index_eval(const Layout& l, int which, int idx_bytes) {
+  if (idx_bytes != 4 && idx_bytes != 8) throw std::invalid_argument("idx_bytes must be 4 or 8");
+  KernelPlan k;
+  bool wide = false;
+  std::string info;
+  std::string fns;
+  long long n = which == 0 ? l.size() : l.phys_size();
+  if (idx_bytes == 4 && std::max(l.size(), l.phys_size()) > (1ll << 31))
+    throw std::invalid_argument("int32 output cannot hold this layout's indices");
+  if (which == 0) {
+    fns = emit_all({{"lego_map", [&](Ctx& c) { return spec_apply_flat(c, l); }}}, &wide, &info);
+  } else {
+    fns = emit_all({{"lego_inv",
+                     [&](Ctx& c) {
+                       FnSpec f = spec_inv_flat(c, l);
+                       f.out_array = true;
+                       return f;
+                     }}},
+                   &wide, &info);
+  }
+  std::ostringstream s;
+  s << header() << "#define IDX_T " << (wide ? "i64" : "u32") << "\n#define OUT_T "
+    << (idx_bytes == 4 ? "int" : "long long") << "\n#define RANK " << l.dims().size() << "\n#define NPOINTS "
+    << n << "ull\n#define " << (which == 0 ? "LEGO_HAVE_APPLY" : "LEGO_HAVE_INV") << " 1\n"
+    << fns << "// ---- template ----\n" << tpl_index_eval;
+  k.src = s.str();
+  k.kernel = which == 0 ? "lego_apply_all" : "lego_inv_all";
+  k.block = 256;
+  k.grid = std::max(1ll, std::min((n + 255) / 256, 256ll * 64));
+  k.info = std::string(which == 0 ? "apply" : "inv") + (wide ? " i64" : " u32") + info;
+  return k;
+}
+
+namespace {
+
+struct Dg {
+  i64 a, b, c;  // destination weight, size, source weight
+  bool tile = false;
+};
+
+// Split digit k at factor f: (a, f, c) and (a*f, b/f, c*f).
+void split_digit(std::vector<Dg>& d, size_t k, i64 f) {
+  Dg lo = d[k], hi = d[k];
+  lo.b = f;
+  hi.a = d[k].a * f;
+  hi.b = d[k].b / f;
+  hi.c = d[k].c * f;
+  d[k] = lo;
+  d.insert(d.begin() + k + 1, hi);
+}
+
+// Mark the lowest digits (by destination weight if by_dst, else by source
+// weight) until their product reaches `target`, splitting one digit if needed.
+void take_lowest(std::vector<Dg>& d, i64 target, bool by_dst) {
+  i64 cum = 1;
+  for (;;) {
+    std::vector<size_t> order(d.size());
+    for (size_t k = 0; k < d.size(); ++k) order[k] = k;
+    std::sort(order.begin(), order.end(), [&](size_t x, size_t y) { return by_dst ? d[x].a < d[y].a : d[x].c < d[y].c; });
+    cum = 1;
+    bool again = false;
+    for (size_t k : order) {
+      if (cum >= target) break;
+      if (cum * d[k].b <= target) {
+        d[k].tile = true;
+        cum *= d[k].b;
+        continue;
+      }
+      i64 need = target / cum;
+      if (target % cum == 0 && need > 1 && d[k].b % need == 0) {
+        split_digit(d, k, need);
+        again = true;  // indices changed; re-run the selection
+      } else {
+        d[k].tile = true;
+        cum *= d[k].b;
+      }
+      break;
+    }
+    if (!again) return;
+  }
+}
+
+i64 tile_size(const std::vector<Dg>& d) {
+  i64 t = 1;
+  for (auto& x : d)
+    if (x.tile) t *= x.b;
+  return t;
+}
+
+int pow2_vec(i64 run, int max_elems) {
+  int v = 1;
+  while (v * 2 <= max_elems && run % (v * 2) == 0) v *= 2;
+  return v;
+}
+
+}  // namespace
+
+static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_bytes, bool allow_lds);
+
+RemapPlan plan_remap(const Layout& src, const Layout& dst, int elem_bytes) {
+  try {
+    return plan_remap_impl(src, dst, elem_bytes, true);
+  } catch (const Unsupported&) {
+    // No LDS tiling fits this digit structure: fall back to the direct/gather kernel.
+    return plan_remap_impl(src, dst, elem_bytes, false);
+  }
+}
+
+static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_bytes, bool allow_lds) {
+  const char* et = elem_type(elem_bytes);
+  if (src.dims() != dst.dims()) throw std::length_error("remap layouts have different logical shapes");
+  if (src.expand_inner || dst.expand_inner) throw Unsupported("remap of ExpandBy layouts is not supported");
+  const i64 N = src.size();
+  const int maxv = std::max(1, 16 / elem_bytes);
+  RemapPlan R;
+
+  // M(p) = L_src.apply(L_dst.inv(p)) in the canonical digit form.
+  Ctx c0;
+  int p = c0.var("p", N);
+  Sum M = remap_map(c0, src, dst, p);
+  std::vector<Digit> digits;
+  bool pure = digits_of(c0, M, p, &digits);
+
+  i64 run = 1;
+  if (pure) {
+    for (auto& d : digits)
+      if (d.a == 1 && d.coeff == 1) run = d.b;
+  }
+
+  // Direct-path vector width: the largest V with M(V t + e) = M(V t) + e and
+  // M(V t) a multiple of V, proven on the expressions (works for any layout).
+  int V = 1;
+  for (int v = maxv; v >= 2; v /= 2) {
+    if (N % v) continue;
+    Ctx c;
+    int t = c.var("t", N / v), e = c.var("e", v);
+    Sum pe = add(c, mulc(c, var(c, t), v), var(c, e));
+    Sum m = subst(c, remap_map(c, src, dst, c.var("p", N)), (int)c.vars.size() - 1, pe);
+    Sum ep, tp;
+    if (!split_by(m, {e}, &ep, &tp)) continue;
+    if (key(ep) != key(var(c, e))) continue;
+    bool ok = tp.c0 % v == 0;
+    for (auto& tt : tp.t) ok = ok && tt.c % v == 0;
+    if (ok) {
+      V = v;
+      break;
+    }
+  }
+  if (!pure) run = V;
+  R.run = run;
+
+  const bool long_run = run * elem_bytes >= 128 || run == N;
+  if (V * elem_bytes >= 16 && (long_run || !pure)) {
+    // ---- direct path
+    R.path = REMAP_DIRECT;
+  } else if (pure && N >= 64 && allow_lds) {
+    R.path = REMAP_LDS;
+  } else {
+    R.path = V > 1 ? REMAP_DIRECT : REMAP_GATHER;
+  }
+
+  std::ostringstream s;
+  std::string info;
+  bool wide = false;
+  const int nontemporal = 1;
+  if (R.path == REMAP_DIRECT || R.path == REMAP_GATHER) {
+    const int NT = 256, UNROLL = V >= maxv ? 4 : 8;
+    const i64 nvec = N / V;
+    std::string fns = emit_all({{"src_vec",
+                                 [&](Ctx& c) {
+                                   int t = c.var("t", nvec);
+                                   int pv = c.var("p", N);
+                                   Sum m = subst(c, remap_map(c, src, dst, pv), pv, mulc(c, var(c, t), V));
+                                   FnSpec f;
+                                   f.params = {t};
+                                   f.outs = {fdiv(c, m, V)};
+                                   return f;
+                                 }}},
+                               &wide, &info);
+    s << header() << "#define ELEM_T " << et << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define V " << V
+      << "\n#define NVEC " << nvec << "ull\n#define NT " << NT << "\n#define UNROLL " << UNROLL
+      << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_DIRECT 1\n"
+      << fns << "// ---- template ----\n" << tpl_remap;
+    R.kernel = "lego_remap_direct";
+    R.block = NT;
+    R.grid = (nvec + (long long)NT * UNROLL - 1) / ((long long)NT * UNROLL);
+    R.vec = V;
+    R.vec_dst = V;
+    R.src = s.str();
+    R.info = std::string(R.path == REMAP_DIRECT ? "direct" : "gather") + " V=" + std::to_string(V) +
+             " run=" + std::to_string(run) + info;
+    return R;
+  }
+
+  // ---- LDS path: choose the tile digits.
+  std::vector<Dg> d;
+  for (auto& x : digits) d.push_back({x.a, x.b, x.coeff});
+  const i64 max_tile = std::min<i64>(N, (32 * 1024) / elem_bytes);
+  i64 tdst = std::min<i64>(N, std::max<i64>(maxv, 256 / elem_bytes));
+  i64 tsrc = std::min<i64>(N, std::max<i64>(maxv, 256 / elem_bytes));
+  take_lowest(d, tdst, true);
+  take_lowest(d, tsrc, false);
+  // Grow the tile toward 16 KiB by alternately extending both sides.
+  for (int step = 0; step < 16 && tile_size(d) * elem_bytes < 16 * 1024; ++step) {
+    std::vector<Dg> trial = d;
+    if (step % 2 == 0)
+      tdst *= 2;
+    else
+      tsrc *= 2;
+    take_lowest(trial, step % 2 == 0 ? tdst : tsrc, step % 2 == 0);
+    if (tile_size(trial) > max_tile) break;
+    d = trial;
+  }
+  std::sort(d.begin(), d.end(), [](const Dg& x, const Dg& y) { return x.a < y.a; });
+  const i64 TILE = tile_size(d);
+  const i64 G = N / TILE;
+  // Tile-local orders.
+  std::vector<size_t> td, ts, gd;
+  for (size_t k = 0; k < d.size(); ++k) (d[k].tile ? td : gd).push_back(k);
+  ts = td;
+  std::sort(ts.begin(), ts.end(), [&](size_t x, size_t y) { return d[x].c < d[y].c; });
+  std::vector<i64> wd(d.size()), ws(d.size()), wg(d.size());
+  i64 w = 1;
+  for (size_t k : td) {
+    wd[k] = w;
+    w *= d[k].b;
+  }
+  w = 1;
+  for (size_t k : ts) {
+    ws[k] = w;
+    w *= d[k].b;
+  }
+  w = 1;
+  for (size_t k : gd) {
+    wg[k] = w;
+    w *= d[k].b;
+  }
+  // Vector widths: the leading tile digits that are contiguous on the source
+  // (destination) side form runs; vectors must divide those runs.
+  i64 srun = 1, drun = 1;
+  for (size_t k : ts) {
+    if (d[k].c != srun) break;
+    srun *= d[k].b;
+  }
+  for (size_t k : td) {
+    if (d[k].a != drun) break;
+    drun *= d[k].b;
+  }
+  const int VL = pow2_vec(srun, maxv);
+  const int VS = pow2_vec(drun, maxv);
+  // LDS tile rows: the lowest destination digits up to 64 elements form one
+  // row; vectors of VS are XOR-swizzled across rows (the swizzle is itself a
+  // GenP layout over [TILE/W, W]) to spread the scattered source-order writes
+  // over banks.
+  i64 W = 1;
+  for (size_t k : td) {
+    if (W * d[k].b > std::max<i64>(64, VS)) break;
+    W *= d[k].b;
+  }
+  while (W < VS) W *= 2;
+  bool swz = W / VS >= 2 && ((W / VS) & (W / VS - 1)) == 0 && TILE % W == 0;
+  PieceP sw = swz ? make_genp(GEN_XOR_SWIZZLE, {TILE / W, W}, {VS, 1}) : make_row({TILE / W, W});
+  LayoutP swl = make_from_piece(sw);
+
+  auto digit_of = [&](Ctx& c, const Sum& x, i64 weight, i64 b) { return fmod(c, fdiv(c, x, weight), b); };
+  auto kd_from_ks = [&](Ctx& c, const Sum& ks) {
+    Sum kd = cst(0);
+    for (size_t k : ts) kd = add(c, kd, mulc(c, digit_of(c, ks, ws[k], d[k].b), wd[k]));
+    return kd;
+  };
+  auto lds_slot = [&](Ctx& c, const Sum& kd) {
+    SymAlg al{&c};
+    return swl->apply(al, {fdiv(c, kd, W), fmod(c, kd, W)});
+  };
+  auto group_part = [&](Ctx& c, int g, bool dst_side) {
+    Sum o = cst(0);
+    for (size_t k : gd) o = add(c, o, mulc(c, digit_of(c, var(c, g), wg[k], d[k].b), dst_side ? d[k].a : d[k].c));
+    return o;
+  };
+  std::string fns = emit_all(
+      {{"src_off",
+        [&](Ctx& c) {
+          int g = c.var("g", G), q = c.var("q", TILE / VL);
+          Sum ks = mulc(c, var(c, q), VL);
+          Sum o = group_part(c, g, false);
+          for (size_t k : ts) o = add(c, o, mulc(c, digit_of(c, ks, ws[k], d[k].b), d[k].c));
+          FnSpec f;
+          f.params = {g, q};
+          f.outs = {o};
+          return f;
+        }},
+       {"ldsw",
+        [&](Ctx& c) {
+          int q = c.var("q", TILE / VL), e = c.var("e", VL);
+          Sum ks = add(c, mulc(c, var(c, q), VL), var(c, e));
+          FnSpec f;
+          f.params = {q, e};
+          f.outs = {lds_slot(c, kd_from_ks(c, ks))};
+          return f;
+        }},
+       {"ldsr",
+        [&](Ctx& c) {
+          int q = c.var("q", TILE / VS);
+          FnSpec f;
+          f.params = {q};
+          f.outs = {lds_slot(c, mulc(c, var(c, q), VS))};
+          return f;
+        }},
+       {"dst_off",
+        [&](Ctx& c) {
+          int g = c.var("g", G), q = c.var("q", TILE / VS);
+          Sum kd = mulc(c, var(c, q), VS);
+          Sum o = group_part(c, g, true);
+          for (size_t k : td) o = add(c, o, mulc(c, digit_of(c, kd, wd[k], d[k].b), d[k].a));
+          FnSpec f;
+          f.params = {g, q};
+          f.outs = {o};
+          return f;
+        }}},
+      &wide, &info);
+  // Are the VL elements of a source vector contiguous in LDS?
+  bool contig = false;
+  {
+    Ctx c;
+    int q = c.var("q", TILE / VL), e = c.var("e", VL);
+    Sum slot = lds_slot(c, kd_from_ks(c, add(c, mulc(c, var(c, q), VL), var(c, e))));
+    Sum ep, qp;
+    if (split_by(slot, {e}, &ep, &qp) && key(ep) == key(var(c, e))) {
+      contig = qp.c0 % VL == 0;
+      for (auto& t : qp.t) contig = contig && t.c % VL == 0;
+    }
+  }
+  int NT = (int)std::min<i64>(256, std::min<i64>(TILE / VL, TILE / VS));
+  if (NT < 1 || (TILE / VL) % NT || (TILE / VS) % NT) throw Unsupported("LDS tile does not divide into vectors");
+  s << header() << "#define ELEM_T " << et << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define TILE " << TILE
+    << "\n#define NELEM " << N << "ull\n#define NTILES " << G << "ull\n#define NT " << NT << "\n#define VL " << VL << "\n#define VS " << VS << "\n#define LDSW_CONTIG "
+    << (contig ? 1 : 0) << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_LDS 1\n"
+    << fns << "// ---- template ----\n" << tpl_remap;
+  R.kernel = "lego_remap_lds";
+  R.block = NT;
+  R.grid = G;
+  R.vec = VL;
+  R.vec_dst = VS;
+  R.tile = TILE;
+  R.src = s.str();
+  R.info = "lds TILE=" + std::to_string(TILE) + " VL=" + std::to_string(VL) + " VS=" + std::to_string(VS) +
+           " W=" + std::to_string(W) + (swz ? " xor" : " row") + (contig ? " contig" : " scatter") +
+           " run=" + std::to_string(run) + info;
+  return R;
+}
+
+}  // namespace lego

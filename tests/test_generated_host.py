@@ -1,0 +1,341 @@
+"""Host execution of the generated index code ("fake device").
+
+Every generated kernel source of the built-in configurations is cut before its
+kernel template; the lowered index functions are compiled with g++ and run on
+the CPU exactly as the kernels call them.  The harness checks that every
+address stays inside its buffer and that every map is a bijection, and it
+simulates the data movement the kernel performs (index maps, remaps) so the
+result can be compared element by element with the oracle.  This catches
+lowering and planning bugs before any GPU launch.
+"""
+import os
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+
+from oracle import layout as OL
+from oracle import remap as OR
+
+MARK = "// ---- template ----"
+
+HARNESS_COMMON = r"""
+#define LEGO_FN static inline
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+#define FAIL(...) do { fprintf(stderr, __VA_ARGS__); fprintf(stderr, "\n"); exit(1); } while (0)
+"""
+
+HARNESS_INDEX = r"""
+int main(int argc, char** argv) {
+  FILE* f = fopen(argv[1], "wb");
+#ifdef LEGO_HAVE_APPLY
+  for (u64 x = 0; x < NPOINTS; ++x) { long long v = (long long)lego_map((IDX_T)x); fwrite(&v, 8, 1, f); }
+#else
+  for (u64 p = 0; p < NPOINTS; ++p) {
+    IDX_T o[RANK]; lego_inv((IDX_T)p, o);
+    for (int k = 0; k < RANK; ++k) { long long v = (long long)o[k]; fwrite(&v, 8, 1, f); }
+  }
+#endif
+  fclose(f);
+  return 0;
+}
+"""
+
+HARNESS_REMAP = r"""
+int main(int argc, char** argv) {
+#ifdef LEGO_REMAP_DIRECT
+  const u64 n = NVEC * (u64)V;
+  std::vector<long long> perm(n, -1);  // dst element -> src element
+  for (u64 t = 0; t < NVEC; ++t) {
+    u64 s = (u64)src_vec((IDX_T)t);
+    if (s >= NVEC) FAIL("src_vec(%llu) = %llu out of range", (unsigned long long)t, (unsigned long long)s);
+    for (int e = 0; e < V; ++e) perm[t * V + e] = (long long)(s * V + e);
+  }
+#else
+  const u64 n = NELEM;
+  std::vector<long long> perm(n, -1);
+  std::vector<long long> tile(TILE);
+  std::vector<char> wseen(TILE);
+  for (u64 g = 0; g < NTILES; ++g) {
+    std::fill(tile.begin(), tile.end(), -1);
+    for (u64 q = 0; q < TILE / VL; ++q) {
+      u64 s = (u64)src_off((IDX_T)g, (IDX_T)q);
+      if (s % VL || s + VL > n) FAIL("src_off(%llu,%llu) = %llu bad", (unsigned long long)g, (unsigned long long)q, (unsigned long long)s);
+      for (int e = 0; e < VL; ++e) {
+        u64 l = (u64)ldsw((IDX_T)q, (IDX_T)e);
+        if (l >= TILE) FAIL("ldsw out of range");
+        if (g == 0) { if (wseen[l]++) FAIL("ldsw not injective"); }
+        tile[l] = (long long)(s + e);
+      }
+    }
+    for (u64 q = 0; q < TILE / VS; ++q) {
+      u64 l = (u64)ldsr((IDX_T)q);
+      u64 d = (u64)dst_off((IDX_T)g, (IDX_T)q);
+      if (l % VS || l + VS > TILE) FAIL("ldsr out of range");
+      if (d % VS || d + VS > n) FAIL("dst_off out of range");
+      for (int e = 0; e < VS; ++e) {
+        if (perm[d + e] != -1) FAIL("destination written twice");
+        if (tile[l + e] < 0) FAIL("LDS slot read before written");
+        perm[d + e] = tile[l + e];
+      }
+    }
+  }
+#endif
+  std::vector<char> seen(n);
+  for (u64 i = 0; i < n; ++i) {
+    if (perm[i] < 0) FAIL("destination %llu never written", (unsigned long long)i);
+    if (seen[perm[i]]++) FAIL("source read twice");
+  }
+  FILE* f = fopen(argv[1], "wb");
+  fwrite(perm.data(), 8, n, f);
+  fclose(f);
+  return 0;
+}
+"""
+
+HARNESS_GEMM = r"""
+static u64 goff_a(u64 tm, u64 kt, u64 tid, u64 u) {
+#if A_SEP
+  return (u64)a_gt((IDX_T)tm) + (u64)a_gk((IDX_T)kt) + (u64)a_gl((IDX_T)tid, (IDX_T)u);
+#else
+  return (u64)a_gf((IDX_T)tm, (IDX_T)kt, (IDX_T)tid, (IDX_T)u);
+#endif
+}
+static u64 goff_b(u64 tn, u64 kt, u64 tid, u64 u) {
+#if B_SEP
+  return (u64)b_gt((IDX_T)tn) + (u64)b_gk((IDX_T)kt) + (u64)b_gl((IDX_T)tid, (IDX_T)u);
+#else
+  return (u64)b_gf((IDX_T)tn, (IDX_T)kt, (IDX_T)tid, (IDX_T)u);
+#endif
+}
+int main() {
+  // schedule: a bijection of workgroups onto tiles
+  std::vector<char> seen(GEMM_MT * GEMM_NT);
+  for (u64 pid = 0; pid < GEMM_MT * GEMM_NT; ++pid) {
+    IDX_T tm, tn; sched((IDX_T)pid, &tm, &tn);
+    if ((u64)tm >= GEMM_MT || (u64)tn >= GEMM_NT) FAIL("sched out of range");
+    if (seen[(u64)tm * GEMM_NT + tn]++) FAIL("sched not injective");
+  }
+  // global loads: every element of A (B) loaded exactly once per tile row (column)
+  {
+    std::vector<char> a(GEMM_M * GEMM_K);
+    for (u64 tm = 0; tm < GEMM_MT; ++tm) for (u64 kt = 0; kt < KT; ++kt)
+      for (u64 tid = 0; tid < NT; ++tid) for (u64 u = 0; u < A_NV; ++u) {
+        if (A_GUARD && u * NT + tid >= A_NVEC) continue;
+        u64 o = goff_a(tm, kt, tid, u);
+        if (o % A_V || o + A_V > GEMM_M * GEMM_K) FAIL("A offset out of range");
+        for (int e = 0; e < A_V; ++e) if (a[o + e]++) FAIL("A element loaded twice");
+      }
+    for (char c : a) if (c != 1) FAIL("A element never loaded");
+  }
+  {
+    std::vector<char> b(GEMM_K * GEMM_N);
+    for (u64 tn = 0; tn < GEMM_NT; ++tn) for (u64 kt = 0; kt < KT; ++kt)
+      for (u64 tid = 0; tid < NT; ++tid) for (u64 u = 0; u < B_NV; ++u) {
+        if (B_GUARD && u * NT + tid >= B_NVEC) continue;
+        u64 o = goff_b(tn, kt, tid, u);
+        if (o % B_V || o + B_V > GEMM_K * GEMM_N) FAIL("B offset out of range");
+        for (int e = 0; e < B_V; ++e) if (b[o + e]++) FAIL("B element loaded twice");
+      }
+    for (char c : b) if (c != 1) FAIL("B element never loaded");
+  }
+  // LDS stores: a bijection onto each stage
+  {
+    std::vector<char> la(BM * BK), lb(BN * BK);
+    for (u64 tid = 0; tid < NT; ++tid) {
+      for (u64 u = 0; u < A_NV; ++u) {
+        if (A_GUARD && u * NT + tid >= A_NVEC) continue;
+        for (int e = 0; e < A_V; ++e) { u64 o = a_s((IDX_T)tid, (IDX_T)u, (IDX_T)e); if (o >= BM * BK || la[o]++) FAIL("a_s bad"); }
+      }
+      for (u64 u = 0; u < B_NV; ++u) {
+        if (B_GUARD && u * NT + tid >= B_NVEC) continue;
+        for (int e = 0; e < B_V; ++e) { u64 o = b_s((IDX_T)tid, (IDX_T)u, (IDX_T)e); if (o >= BN * BK || lb[o]++) FAIL("b_s bad"); }
+      }
+    }
+    for (char c : la) if (c != 1) FAIL("LDS A slot never written");
+    for (char c : lb) if (c != 1) FAIL("LDS B slot never written");
+  }
+  // fragment reads stay inside the stage; each wave reads its rows x all k
+  for (u64 w = 0; w < NWAVES; ++w) {
+    std::vector<int> ra(BM * BK), rb(BN * BK);
+    for (u64 lane = 0; lane < 64; ++lane) for (u64 s = 0; s < BK / KB; ++s) for (int e = 0; e < 8; ++e) {
+      for (u64 mi = 0; mi < MI; ++mi) { u64 o = a_fr((IDX_T)lane, (IDX_T)w, (IDX_T)mi, (IDX_T)s, (IDX_T)e); if (o >= BM * BK) FAIL("a_fr out of range"); ra[o]++; }
+      for (u64 ni = 0; ni < NI; ++ni) { u64 o = b_fr((IDX_T)lane, (IDX_T)w, (IDX_T)ni, (IDX_T)s, (IDX_T)e); if (o >= BN * BK) FAIL("b_fr out of range"); rb[o]++; }
+    }
+    long long na = 0, nb = 0;
+    for (int c : ra) { if (c > 1) FAIL("a_fr duplicates"); na += c != 0; }
+    for (int c : rb) if (c > 1) FAIL("b_fr duplicates");
+    for (int c : rb) nb += c != 0;
+    if (na != (long long)MI * MB * BK || nb != (long long)NI * MB * BK) FAIL("fragments do not cover the wave tile");
+  }
+  // epilogue: every C element written exactly once
+  {
+    std::vector<char> c(GEMM_M * GEMM_N);
+    for (u64 tm = 0; tm < GEMM_MT; ++tm) for (u64 tn = 0; tn < GEMM_NT; ++tn)
+      for (u64 lane = 0; lane < 64; ++lane) for (u64 w = 0; w < NWAVES; ++w)
+        for (u64 mi = 0; mi < MI; ++mi) for (u64 ni = 0; ni < NI; ++ni) for (u64 r = 0; r < (MB == 32 ? 16 : 4); ++r) {
+#if C_SEP
+          u64 o = (u64)c_t((IDX_T)tm, (IDX_T)tn) + (u64)c_l((IDX_T)lane, (IDX_T)w, (IDX_T)mi, (IDX_T)ni, (IDX_T)r);
+#else
+          u64 o = (u64)c_f((IDX_T)tm, (IDX_T)tn, (IDX_T)lane, (IDX_T)w, (IDX_T)mi, (IDX_T)ni, (IDX_T)r);
+#endif
+          if (o >= GEMM_M * GEMM_N || c[o]++) FAIL("C offset bad");
+        }
+  }
+  printf("ok\n");
+  return 0;
+}
+"""
+
+
+def _sources():
+    import paper_2505_08091_amd as L
+    return L.selftest_sources()
+
+
+def _oracle_for(name):
+    """Oracle layouts (and element size) behind each built-in generated source."""
+    c1 = OL.TileOrderBy(OL.Row(2, 2), OL.Row(4, 4), OL.Row(16, 16))
+    row8 = OL.as_layout(OL.Row(8192, 8192))
+    blk = OL.TileOrderBy(OL.Col(128, 128), OL.Row(64, 64))
+    r4 = OL.as_layout(OL.Row(4096, 4096))
+    mz = OL.as_layout(OL.morton_genp(4096, 4096))
+    return {
+        "index apply 128x128 tiled": ("apply", c1),
+        "index inv 128x128 tiled": ("inv", c1),
+        "remap row->blocked f32": ("remap", row8, blk),
+        "remap blocked->row f32": ("remap", blk, row8),
+        "remap row->morton f16": ("remap", r4, mz),
+        "remap morton->row f16": ("remap", mz, r4),
+        "remap row->col f32": ("remap", row8, OL.as_layout(OL.Col(8192, 8192))),
+    }.get(name)
+
+
+def _compile_and_run(src, harness, tmp, args=()):
+    head = src.split(MARK)[0]
+    cpp = os.path.join(tmp, "h.cpp")
+    exe = os.path.join(tmp, "h")
+    with open(cpp, "w") as f:
+        f.write(HARNESS_COMMON + head + harness)
+    r = subprocess.run(["g++", "-O2", "-std=c++17", "-w", cpp, "-o", exe], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-4000:]
+    r = subprocess.run([exe, *args], capture_output=True, text=True, timeout=600)
+    assert r.returncode == 0, r.stderr[-2000:]
+    return r.stdout
+
+
+@pytest.mark.parametrize("i", range(11))
+def test_generated_source_on_host(i):
+    srcs = _sources()
+    if i >= len(srcs):
+        pytest.skip("no such source")
+    name, src = srcs[i]
+    assert MARK in src
+    with tempfile.TemporaryDirectory() as tmp:
+        out = os.path.join(tmp, "out.bin")
+        if "LEGO_HAVE_APPLY" in src or "LEGO_HAVE_INV" in src:
+            kind, lay = _oracle_for(name)
+            _compile_and_run(src, HARNESS_INDEX, tmp, [out])
+            got = np.fromfile(out, dtype=np.int64)
+            if kind == "apply":
+                assert (got == OL.apply_all(lay)).all(), name
+            else:
+                assert (got.reshape(-1, 2) == OL.inv_all(lay)).all(), name
+        elif "LEGO_REMAP_" in src:
+            kind, ls, ld = _oracle_for(name)
+            _compile_and_run(src, HARNESS_REMAP, tmp, [out])
+            perm = np.fromfile(out, dtype=np.int64)
+            # the oracle moves element indices: dst[L_dst(x)] = src[L_src(x)]
+            exp = OR.remap(ls, ld, np.arange(ls.size(), dtype=np.int64))
+            assert (perm == exp).all(), name
+        else:
+            assert "lego_gemm" in src
+            assert _compile_and_run(src, HARNESS_GEMM, tmp).strip() == "ok", name
+
+
+# ------------------------------------------------------------------------
+# Every configuration the GPU tests launch, checked on the host first.
+def _index_cases():
+    import paper_2505_08091_amd as L
+    from tests.test_gpu_index import _cases
+    return _cases(L)
+
+
+def test_index_sources_of_gpu_cases():
+    import paper_2505_08091_amd as L
+    with tempfile.TemporaryDirectory() as tmp:
+        out = os.path.join(tmp, "out.bin")
+        for name, lay, olay in _index_cases():
+            for kind in ("apply", "inv"):
+                src = L.plan_source(kind, lay, param=8)
+                _compile_and_run(src, HARNESS_INDEX, tmp, [out])
+                got = np.fromfile(out, dtype=np.int64)
+                if kind == "apply":
+                    assert (got == OL.apply_all(olay)).all(), name
+                else:
+                    assert (got.reshape(-1, len(olay.dims())) == OL.inv_all(olay)).all(), name
+
+
+def _remap_cases():
+    import paper_2505_08091_amd as L
+    from tests.test_gpu_remap import _small_cases
+    cases = [(n, ls, ld, ols, old) for n, ls, ld, ols, old in _small_cases(L)]
+    for n in (2048, 4096, 1024):
+        cases.append((f"transpose {n}", L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n)),
+                      OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.Col(n, n))))
+    cases.append(("identity 8192", L.as_layout(L.Row(8192, 8192)), L.as_layout(L.Row(8192, 8192)),
+                  OL.as_layout(OL.Row(8192, 8192)), OL.as_layout(OL.Row(8192, 8192))))
+    return cases
+
+
+@pytest.mark.parametrize("elem_bytes", [1, 2, 4, 8])
+def test_remap_sources_of_gpu_cases(elem_bytes):
+    import paper_2505_08091_amd as L
+    with tempfile.TemporaryDirectory() as tmp:
+        out = os.path.join(tmp, "out.bin")
+        for name, ls, ld, ols, old in _remap_cases():
+            if ols.size() > (1 << 23) and elem_bytes != 4:
+                continue
+            for a, b, oa, ob in ((ls, ld, ols, old), (ld, ls, old, ols)):
+                src = L.plan_source("remap", a, b, param=elem_bytes)
+                _compile_and_run(src, HARNESS_REMAP, tmp, [out])
+                perm = np.fromfile(out, dtype=np.int64)
+                exp = OR.remap(oa, ob, np.arange(oa.size(), dtype=np.int64))
+                assert (perm == exp).all(), (name, elem_bytes)
+
+
+def _gemm_cases():
+    import paper_2505_08091_amd as L
+    cases = []
+    for dt in ("f16", "bf16"):
+        cases.append(dict(M=128, N=128, K=128, dtype=dt, bm=64, bn=64, bk=32, wm=16, wn=16))
+    cases.append(dict(M=1024, N=1024, K=1024, dtype="f16", bm=128, bn=128, bk=32, wm=64, wn=64, group_m=8))
+    cases.append(dict(M=512, N=768, K=1024, dtype="bf16"))
+    for la in ("Row", "Col"):
+        for lb in ("Row", "Col"):
+            cases.append(dict(M=256, N=512, K=384, dtype="f16", a=L.as_layout(getattr(L, la)(256, 384)),
+                              b=L.as_layout(getattr(L, lb)(384, 512)), c=L.as_layout(L.Col(256, 512)),
+                              bm=128, bn=128, bk=64, wm=64, wn=64))
+    cases.append(dict(M=64, N=64, K=64, dtype="f16", bm=64, bn=64, bk=32, wm=32, wn=32))
+    cases.append(dict(M=64, N=64, K=64, dtype="f16", bm=64, bn=64, bk=32, wm=16, wn=16))
+    cases.append(dict(M=8192, N=8192, K=8192, dtype="bf16"))
+    cases.append(dict(M=4096, N=4096, K=4096, dtype="f16", a=L.as_layout(L.GenP("morton", [4096, 4096])),
+                      b=L.as_layout(L.Row(4096, 4096))))
+    cases.append(dict(M=256, N=256, K=256, dtype="f16", bm=128, bn=128, bk=32, wm=64, wn=64))  # smoke
+    return cases
+
+
+@pytest.mark.parametrize("i", range(14))
+def test_gemm_sources_of_gpu_cases(i):
+    import paper_2505_08091_amd as L
+    cases = _gemm_cases()
+    if i >= len(cases):
+        pytest.skip("no such case")
+    kw = cases[i]
+    src = L.plan_source("gemm", **kw)
+    with tempfile.TemporaryDirectory() as tmp:
+        assert _compile_and_run(src, HARNESS_GEMM, tmp).strip() == "ok", kw

@@ -1,0 +1,157 @@
+"""GEMM on the gfx950 matrix cores against the fp64 oracle.
+
+Tolerance (fp16/bf16 inputs, fp32 accumulation, fp32 C): per element
+|C - R| / max(|R|, ||R||_F / sqrt(MN)) <= 2e-2 and ||C - R||_F / ||R||_F <= 1e-3.
+Small-integer inputs make every partial sum exact in fp32, so that case must
+match the oracle bit for bit.
+"""
+import numpy as np
+import pytest
+
+import synth_inputs as S
+from oracle import gemm as OG
+from oracle import layout as OL
+from tests.gpu_util import need_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(lego, a_buf, b_buf, M, N, K, dtype, **kw):
+    import torch
+    dev = need_gpu()
+    c = torch.full((M * N,), float("nan"), dtype=torch.float32, device=dev)
+    lego.gemm(a_buf.to(dev), b_buf.to(dev), c, M, N, K, dtype, **kw)
+    torch.cuda.synchronize()
+    return c.cpu().numpy()
+
+
+def _logical_c(c_flat, olc, rows=None):
+    return OG.logical_matrix(c_flat.view(np.float32), olc, "f32", rows)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gemm_c1_128(lego, dtype):
+    """128^3 with 64x64 workgroup tiles of 16x16 wave tiles (16x16x32 MFMA)."""
+    M = N = K = 128
+    a = S.tensor(M * K, dtype, seed=S.SEED_A)
+    b = S.tensor(K * N, dtype, seed=S.SEED_B)
+    kw = dict(bm=64, bn=64, bk=32, wm=16, wn=16)
+    say(f"gemm C1 {dtype} plan={lego.gemm_plan(M, N, K, dtype, **kw)}")
+    c = _run(lego, a, b, M, N, K, dtype, **kw)
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(OL.Row(M, K)), OL.as_layout(OL.Col(K, N)), dtype)
+    ok, mre, fre = OG.check_tolerance(c.reshape(M, N), r)
+    assert ok, (mre, fre)
+
+
+def test_gemm_c3_1024_f16(lego):
+    """1024^3 fp16, A Row, B Col, 128x128x32 tiles, 64x64 wave tiles, grouped order."""
+    M = N = K = 1024
+    a = S.tensor(M * K, "f16", seed=S.SEED_A)
+    b = S.tensor(K * N, "f16", seed=S.SEED_B)
+    kw = dict(bm=128, bn=128, bk=32, wm=64, wn=64, group_m=8)
+    say(f"gemm C3 plan={lego.gemm_plan(M, N, K, 'f16', **kw)}")
+    c = _run(lego, a, b, M, N, K, "f16", **kw)
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(OL.Row(M, K)), OL.as_layout(OL.Col(K, N)), "f16")
+    ok, mre, fre = OG.check_tolerance(c.reshape(M, N), r)
+    assert ok, (mre, fre)
+
+
+def test_gemm_exact_small_integers(lego):
+    """Inputs in {-2..2}: the fp32 result is exact, so it must equal the oracle."""
+    M, N, K = 512, 768, 1024
+    a = S.tensor(M * K, "bf16", dist="smallint", seed=11)
+    b = S.tensor(K * N, "bf16", dist="smallint", seed=12)
+    say("gemm exact small-int 512x768x1024 bf16")
+    c = _run(lego, a, b, M, N, K, "bf16")
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(OL.Row(M, K)), OL.as_layout(OL.Col(K, N)), "bf16")
+    assert (c.reshape(M, N) == r).all()
+
+
+def test_gemm_layout_variants(lego):
+    """The four Row/Col variants of A and B (Section V-A) and a column-major C."""
+    M, N, K = 256, 512, 384
+    a = S.tensor(M * K, "f16", seed=S.SEED_A)
+    b = S.tensor(K * N, "f16", seed=S.SEED_B)
+    for la_name in ("Row", "Col"):
+        for lb_name in ("Row", "Col"):
+            la = getattr(lego, la_name)(M, K)
+            lb = getattr(lego, lb_name)(K, N)
+            ola = getattr(OL, la_name)(M, K)
+            olb = getattr(OL, lb_name)(K, N)
+            lc = lego.as_layout(lego.Col(M, N))
+            kw = dict(a=lego.as_layout(la), b=lego.as_layout(lb), c=lc, bm=128, bn=128, bk=64, wm=64, wn=64)
+            say(f"gemm A {la_name} B {lb_name} C Col plan={lego.gemm_plan(M, N, K, 'f16', **kw)}")
+            c = _run(lego, a, b, M, N, K, "f16", **kw)
+            r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(ola), OL.as_layout(olb), "f16")
+            got = _logical_c(c, OL.as_layout(OL.Col(M, N)))
+            ok, mre, fre = OG.check_tolerance(got, r)
+            assert ok, (la_name, lb_name, mre, fre)
+
+
+def test_gemm_fragment_probe_one_hot(lego):
+    """A = e_(m,k), B = e_(k,n): C must be exactly 1 at (m, n) and 0 elsewhere,
+    which pins the C/D fragment layout of the MFMA instruction."""
+    import torch
+    M = N = K = 64
+    rng = np.random.default_rng(0)
+    for _ in range(6):
+        m, k, n = (int(x) for x in rng.integers(0, 64, 3))
+        a = torch.zeros(M * K, dtype=torch.float16)
+        b = torch.zeros(K * N, dtype=torch.float16)
+        a[m * K + k] = 1.0
+        b[n * K + k] = 1.0  # B column-major
+        for kw in (dict(bm=64, bn=64, bk=32, wm=32, wn=32), dict(bm=64, bn=64, bk=32, wm=16, wn=16)):
+            say(f"gemm one-hot m={m} k={k} n={n} {kw}")
+            c = _run(lego, a, b, M, N, K, "f16", **kw).reshape(M, N)
+            exp = np.zeros((M, N), dtype=np.float32)
+            exp[m, n] = 1.0
+            assert (c == exp).all(), (m, k, n, kw)
+
+
+def test_gemm_c4_8192_bf16_sampled(lego):
+    """8192^3 bf16 with the default 256x256x64 plan, checked on sampled rows."""
+    M = N = K = 8192
+    a = S.tensor(M * K, "bf16", dist="normal", seed=S.SEED_A)
+    b = S.tensor(K * N, "bf16", dist="normal", seed=S.SEED_B)
+    say(f"gemm C4 plan={lego.gemm_plan(M, N, K, 'bf16')}")
+    c = _run(lego, a, b, M, N, K, "bf16").reshape(M, N)
+    rows = np.random.default_rng(1).choice(M, 48, replace=False)
+    rows = np.concatenate([rows, [0, 255, 256, M - 1]])
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(OL.Row(M, K)), OL.as_layout(OL.Col(K, N)),
+                "bf16", rows=rows)
+    ok, mre, fre = OG.check_tolerance(c[rows], r)
+    assert ok, (mre, fre)
+
+
+def test_gemm_c5_morton_a_sampled(lego):
+    """4096^3 fp16 with A stored in Morton order and B row-major."""
+    import torch
+    M = N = K = 4096
+    a_log = S.tensor(M * K, "f16", seed=S.SEED_A)  # logical row-major values
+    b = S.tensor(K * N, "f16", seed=S.SEED_B)
+    mz = lego.as_layout(lego.GenP("morton", [M, K]))
+    row = lego.as_layout(lego.Row(M, K))
+    dev = need_gpu()
+    a_mz = torch.empty_like(a_log, device=dev)
+    lego.remap(row, mz, a_log.to(dev), a_mz)  # store A in Morton order
+    kw = dict(a=mz, b=lego.as_layout(lego.Row(K, N)))
+    say(f"gemm C5 plan={lego.gemm_plan(M, N, K, 'f16', **kw)}")
+    c = _run(lego, a_mz, b, M, N, K, "f16", **kw).reshape(M, N)
+    rows = np.random.default_rng(2).choice(M, 48, replace=False)
+    omz = OL.as_layout(OL.morton_genp(M, K))
+    r = OG.gemm(S.as_numpy_bits(a_mz.cpu()), S.as_numpy_bits(b), omz, OL.as_layout(OL.Row(K, N)), "f16", rows=rows)
+    ok, mre, fre = OG.check_tolerance(c[rows], r)
+    assert ok, (mre, fre)
+
+
+def test_gemm_errors(lego):
+    import torch
+    dev = need_gpu()
+    a = torch.zeros(100 * 64, dtype=torch.float16, device=dev)
+    c = torch.zeros(100 * 64, dtype=torch.float32, device=dev)
+    with pytest.raises(lego.LegoError) as e:
+        lego.gemm(a, a, c, 100, 64, 64, "f16")  # 100 not a multiple of the tile
+    assert e.value.status == "UNSUPPORTED"
+    with pytest.raises(lego.LegoError) as e:
+        lego.gemm(a, a, c, 64, 64, 64, "f32")
+    assert e.value.status == "INVALID_ARG"

@@ -1,0 +1,121 @@
+"""Remaps on the GPU must equal the oracle byte for byte."""
+import numpy as np
+import pytest
+
+import synth_inputs as S
+from oracle import layout as OL
+from oracle import remap as OR
+from tests.gpu_util import bits, need_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(lego, src_l, dst_l, src, dev):
+    import torch
+    d_src = src.to(dev)
+    d_dst = torch.empty_like(d_src)
+    lego.remap(src_l, dst_l, d_src, d_dst)
+    torch.cuda.synchronize()
+    return d_dst.cpu()
+
+
+def test_remap_c2_row_blocked_roundtrip(lego):
+    """8192^2 fp32 Row -> blocked (64x64 tiles, column-major tile order) and back."""
+    dev = need_gpu()
+    n = 8192
+    src = S.tensor(n * n, "f32", seed=S.SEED_SRC)
+    row, blk = lego.as_layout(lego.Row(n, n)), lego.TileOrderBy(lego.Col(128, 128), lego.Row(64, 64))
+    orow, oblk = OL.as_layout(OL.Row(n, n)), OL.TileOrderBy(OL.Col(128, 128), OL.Row(64, 64))
+    say(f"remap C2 fwd plan={lego.remap_plan(row, blk, 4)['info']}")
+    fwd = _run(lego, row, blk, src, dev)
+    exp = OR.remap(orow, oblk, src.numpy())
+    assert (bits(fwd) == exp.view(np.uint32)).all()
+    say(f"remap C2 inv plan={lego.remap_plan(blk, row, 4)['info']}")
+    back = _run(lego, blk, row, fwd, dev)
+    assert (bits(back) == bits(src)).all()
+
+
+def test_remap_c5_row_morton_roundtrip(lego):
+    """4096^2 fp16 Row -> Morton and back (LDS-staged path)."""
+    dev = need_gpu()
+    n = 4096
+    src = S.tensor(n * n, "f16", seed=S.SEED_SRC)
+    row, mz = lego.as_layout(lego.Row(n, n)), lego.as_layout(lego.GenP("morton", [n, n]))
+    orow, omz = OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.morton_genp(n, n))
+    say(f"remap C5 row->morton plan={lego.remap_plan(row, mz, 2)['info']}")
+    fwd = _run(lego, row, mz, src, dev)
+    exp = OR.remap(orow, omz, S.as_numpy_bits(src))
+    assert (bits(fwd) == exp).all()
+    say(f"remap C5 morton->row plan={lego.remap_plan(mz, row, 2)['info']}")
+    back = _run(lego, mz, row, fwd, dev)
+    assert (bits(back) == bits(src)).all()
+
+
+@pytest.mark.parametrize("n,dtype", [(2048, "f32"), (4096, "f16"), (1024, "bf16")])
+def test_remap_transpose(lego, n, dtype):
+    """Row -> Col (the transpose of Table V) equals a numpy transpose."""
+    dev = need_gpu()
+    src = S.tensor(n * n, dtype, seed=S.SEED_SRC)
+    row, col = lego.as_layout(lego.Row(n, n)), lego.as_layout(lego.Col(n, n))
+    say(f"remap transpose n={n} {dtype} plan={lego.remap_plan(row, col, src.element_size())['info']}")
+    out = _run(lego, row, col, src, dev)
+    assert (bits(out) == bits(src).reshape(n, n).T.ravel()).all()
+
+
+def _small_cases(L):
+    return [
+        ("antidiag chain 6x6 (gather)",
+         L.as_layout(L.Row(6, 6)),
+         L.GroupBy([6, 6]).OrderBy(L.RegP([2, 3, 2, 3], [1, 3, 2, 4])).OrderBy(L.RegP([2, 2], [2, 1]),
+                                                                             L.GenP("antidiag", [3, 3])),
+         OL.as_layout(OL.Row(6, 6)),
+         OL.GroupBy([6, 6]).OrderBy(OL.RegP([2, 3, 2, 3], [1, 3, 2, 4])).OrderBy(OL.RegP([2, 2], [2, 1]),
+                                                                               OL.antidiag_genp(3))),
+        ("ragged 3x5 tiles of 7x3", L.as_layout(L.Row(21, 15)), L.TileOrderBy(L.Col(3, 5), L.Row(7, 3)),
+         OL.as_layout(OL.Row(21, 15)), OL.TileOrderBy(OL.Col(3, 5), OL.Row(7, 3))),
+        ("xor swizzle 256x64", L.as_layout(L.Row(256, 64)), L.as_layout(L.GenP("xor_swizzle", [256, 64], [8, 1])),
+         OL.as_layout(OL.Row(256, 64)), OL.as_layout(OL.xor_swizzle_genp(256, 64, 8, 1))),
+        ("morton 16x16 vs col", L.as_layout(L.Col(16, 16)), L.as_layout(L.GenP("morton", [16, 16])),
+         OL.as_layout(OL.Col(16, 16)), OL.as_layout(OL.morton_genp(16, 16))),
+        ("identity 1x1", L.as_layout(L.Row(1, 1)), L.as_layout(L.Row(1, 1)),
+         OL.as_layout(OL.Row(1, 1)), OL.as_layout(OL.Row(1, 1))),
+        ("odd 1000x3 to col", L.as_layout(L.Row(1000, 3)), L.as_layout(L.Col(1000, 3)),
+         OL.as_layout(OL.Row(1000, 3)), OL.as_layout(OL.Col(1000, 3))),
+        ("3-level blocked 512^2", L.as_layout(L.Row(512, 512)),
+         L.TileOrderBy(L.Col(4, 4), L.Row(4, 4), L.Row(32, 32)),
+         OL.as_layout(OL.Row(512, 512)), OL.TileOrderBy(OL.Col(4, 4), OL.Row(4, 4), OL.Row(32, 32))),
+    ]
+
+
+@pytest.mark.parametrize("elem", ["f32", "f16", "i64", "u8"])
+def test_remap_small_and_ragged(lego, elem):
+    import torch
+    dev = need_gpu()
+    for name, ls, ld, ols, old in _small_cases(lego):
+        n = ols.size()
+        if elem == "i64":
+            src = S.int_tensor(n, bits=64)
+        elif elem == "u8":
+            src = (S.int_tensor(n) % 251).to(torch.uint8)
+        else:
+            src = S.tensor(n, elem, seed=7)
+        say(f"remap {name} {elem} plan={lego.remap_plan(ls, ld, src.element_size())['info']}")
+        out = _run(lego, ls, ld, src, dev)
+        exp = OR.remap(ols, old, bits(src))
+        assert (bits(out) == exp).all(), name
+        back = _run(lego, ld, ls, out, dev)
+        assert (bits(back) == bits(src)).all(), name
+
+
+def test_remap_errors(lego):
+    import torch
+    dev = need_gpu()
+    a = torch.zeros(64, device=dev)
+    b = torch.zeros(64, device=dev)
+    r = lego.as_layout(lego.Row(8, 8))
+    with pytest.raises(lego.LegoError) as e:
+        lego.remap(r, lego.as_layout(lego.Row(4, 16)), a, b)
+    assert e.value.status == "SIZE_MISMATCH"
+    with pytest.raises(lego.LegoError) as e:
+        lego.remap(r, r, a, a)
+    assert e.value.status == "INVALID_ARG"
