@@ -2,6 +2,7 @@
 #include "gemm_plan.hpp"
 
 #include <algorithm>
+#include <cstdlib>
 #include <map>
 #include <mutex>
 #include <sstream>
@@ -53,8 +54,17 @@ namespace {
 
 bool pow2(i64 x) { return x > 0 && (x & (x - 1)) == 0; }
 
+// Default LDS tile layout: 16-byte vectors of a row XOR-permuted by (row/s)
+// mod (k/8).  A b128 fragment read is served 16 lanes (16 rows) at a time over
+// 64 banks of 4 bytes, i.e. a 256-byte bank window holding 256/(2k) rows of k
+// 16-bit elements; keying the XOR on row/s with s = 128/k gives the 16 rows of
+// a phase distinct bank groups (s = 2 for k = 64, 4 for k = 32).
 LayoutP default_lds(i64 rows, i64 k) {
-  if (k % 8 == 0 && pow2(k / 8) && k / 8 >= 2) return make_from_piece(make_genp(GEN_XOR_SWIZZLE, {rows, k}, {8, 1}));
+  if (k % 8 == 0 && pow2(k / 8) && k / 8 >= 2) {
+    i64 s = std::max<i64>(1, 128 / k);
+    if (const char* e = std::getenv("LEGO_GEMM_LDS_S")) s = std::max(1, std::atoi(e));
+    return make_from_piece(make_genp(GEN_XOR_SWIZZLE, {rows, k}, {8, s}));
+  }
   return make_from_piece(make_row({rows, k}));
 }
 
@@ -87,6 +97,7 @@ struct Operand {
   int V = 1, axis = 1, NV = 1;
   i64 NVEC = 0;
   bool guard = false, sep = false, svec = false, frvec = false;
+  bool direct = false;  // load vector q fills LDS slot q (direct global-to-LDS copy)
 };
 
 }  // namespace
@@ -98,8 +109,10 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   if (!rq.bm) rq.bm = (int)std::min<i64>(256, rq.M);
   if (!rq.bn) rq.bn = (int)std::min<i64>(256, rq.N);
   if (!rq.bk) rq.bk = (int)std::min<i64>(64, rq.K);
-  if (!rq.wm) rq.wm = rq.bm >= 64 ? rq.bm / 2 : rq.bm;
-  if (!rq.wn) rq.wn = rq.bn >= 64 ? rq.bn / 2 : rq.bn;
+  // Default wave tiles keep at most 8 MFMA blocks (128 fp32 accumulators) per
+  // wave, so accumulators stay in VGPRs and two waves share each SIMD.
+  if (!rq.wm) rq.wm = rq.bm >= 256 ? 128 : (rq.bm >= 64 ? rq.bm / 2 : rq.bm);
+  if (!rq.wn) rq.wn = rq.bn >= 256 ? 64 : (rq.bn >= 64 ? rq.bn / 2 : rq.bn);
   if (!rq.group_m) rq.group_m = 8;
   const i64 M = rq.M, N = rq.N, K = rq.K;
   const int bm = rq.bm, bn = rq.bn, bk = rq.bk, wm = rq.wm, wn = rq.wn;
@@ -156,6 +169,14 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   // Tile element (i, j) of load vector u of thread tid, plus element e.
   auto load_elem = [&](Ctx& c, const Operand& o, const Sum& tid, const Sum& u, const Sum& e, Sum* i, Sum* j) {
     Sum q = add(c, mulc(c, u, NT), tid);
+    if (o.direct) {
+      // Slot q of the LDS tile holds the elements S^{-1}(8q + e).
+      SymAlg al{&c};
+      std::vector<Sum> ij = o.lds->inv(al, add(c, mulc(c, q, 8), e));
+      *i = ij[0];
+      *j = ij[1];
+      return;
+    }
     if (o.axis == 1) {
       i64 per = o.KD / o.V;
       *i = fdiv(c, q, per);
@@ -229,6 +250,54 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       Sum kk = add(c, mulc(c, var(c, s), KB), k);
       o.frvec = contiguous_in(o.lds->apply(al, {row, kk}), e, 8);
     }
+  }
+
+  // Direct global-to-LDS copies need 16-byte global runs under the inverse
+  // LDS layout and whole rounds of load vectors.
+  bool direct = true;
+  if (const char* e = std::getenv("LEGO_GEMM_DIRECT")) direct = std::atoi(e) != 0;
+  if ((bk / KB) % 2) direct = false;  // the direct loop alternates fragment buffers per substep
+  for (Operand& o : ops) {
+    if (!direct) break;
+    if ((o.R * o.KD) % (8 * NT)) {
+      direct = false;
+      break;
+    }
+    Operand t = o;
+    t.direct = true;
+    t.V = 8;
+    t.NV = (int)(o.R * o.KD / 8 / NT);
+    Ctx c;
+    int tt = c.var("tt", o.is_b ? Nt : Mt), kt = c.var("kt", Kt), tid = c.var("tid", NT), u = c.var("u", t.NV),
+        e = c.var("e", 8);
+    Sum i, j;
+    load_elem(c, t, var(c, tid), var(c, u), var(c, e), &i, &j);
+    if (!contiguous_in(glob_off(c, t, var(c, tt), var(c, kt), i, j), e, 8)) direct = false;
+  }
+  if (direct) {
+    for (Operand& o : ops) {
+      o.direct = true;
+      o.V = 8;
+      o.axis = 1;
+      o.NVEC = o.R * o.KD / 8;
+      o.NV = (int)(o.NVEC / NT);
+      o.guard = false;
+      o.svec = true;
+      Ctx c;
+      int tt = c.var("tt", o.is_b ? Nt : Mt), kt = c.var("kt", Kt), tid = c.var("tid", NT), u = c.var("u", o.NV);
+      Sum i, j;
+      load_elem(c, o, var(c, tid), var(c, u), cst(0), &i, &j);
+      Sum off = glob_off(c, o, var(c, tt), var(c, kt), i, j);
+      Sum pt, r1, pk, pl;
+      o.sep = split_by(off, {tt}, &pt, &r1) && split_by(r1, {kt}, &pk, &pl);
+    }
+  }
+  const i64 stage_bytes = 2ll * (bm + bn) * bk;
+  int nstages = 2;
+  if (direct) {
+    nstages = (int)std::min<i64>(4, (160 * 1024) / stage_bytes);
+    if (const char* e = std::getenv("LEGO_GEMM_STAGES")) nstages = std::atoi(e);
+    nstages = (int)std::max<i64>(2, std::min<i64>(nstages, (160 * 1024) / stage_bytes));
   }
 
   // ----- emit the index functions
@@ -408,6 +477,17 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "NVEC " << o.NVEC << "u\n#define " << P2[k]
       << "GUARD " << (o.guard ? 1 : 0) << "\n";
   }
+  // Two staging register sets when the accumulators live in AGPRs (one wave
+  // per SIMD leaves the VGPRs for them); one otherwise, so two waves fit.
+  int prefetch = (MI * NI * NREG > 128) ? 2 : 1;
+  if (const char* e = std::getenv("LEGO_GEMM_PREFETCH")) prefetch = std::atoi(e) == 2 ? 2 : 1;
+  if (Kt < 2) prefetch = 1;
+  s << "#define PREFETCH " << prefetch << "\n#define DIRECT_LDS " << (direct ? 1 : 0) << "\n#define NSTAGES "
+    << nstages << "\n";
+  const char* store_env = std::getenv("LEGO_GEMM_STORE_AT");
+  int store_at = store_env ? std::atoi(store_env) : (bk / KB) / 2;
+  store_at = std::max(0, std::min(store_at, bk / KB - 1));
+  s << "#define STORE_AT " << store_at << "\n";
   s << "#define C_SEP " << (csep ? 1 : 0) << "\n" << code << "// ---- template ----\n" << tpl_gemm;
 
   GemmPlan g;
@@ -423,7 +503,8 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
        << (ops[0].frvec ? " frvec" : " frscalar") << " B:V" << ops[1].V << (ops[1].axis ? "k" : "n")
        << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
        << (ops[1].frvec ? " frvec" : " frscalar") << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
-       << " lds " << lds_bytes << "B ops" << opsinfo.str();
+       << (direct ? " direct-lds" : " staged") << " stages " << nstages << " lds " << nstages * stage_bytes
+       << "B ops" << opsinfo.str();
   g.info = info.str();
   return g;
 }

@@ -101,11 +101,20 @@ void pack_cached(std::vector<char>* blob) {
 }  // namespace
 
 const std::vector<std::string>& jit_options() {
-  static const std::vector<std::string> opts = {
-      "--offload-arch=gfx950", "-O3", "-std=c++17",
-      // Packed fp32 instructions are disabled for all generated code.
-      "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-  };
+  static const std::vector<std::string> opts = [] {
+    std::vector<std::string> o = {
+        "--offload-arch=gfx950", "-O3", "-std=c++17",
+        // Packed fp32 instructions are disabled for all generated code.
+        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    };
+    // Extra compiler options for tuning experiments (space separated).
+    if (const char* extra = std::getenv("LEGO_JIT_OPTS")) {
+      std::istringstream ss(extra);
+      std::string w;
+      while (ss >> w) o.push_back(w);
+    }
+    return o;
+  }();
   return opts;
 }
 

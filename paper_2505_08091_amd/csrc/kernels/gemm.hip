@@ -16,6 +16,10 @@
 //       vector LDS store, vector fragment read, vectors per tile, and whether
 //       the last round of vectors covers only part of the threads
 //   C_SEP
+//   STORE_AT         k-substep during which the next tile is written to LDS
+//   PREFETCH         1 or 2: K steps between a tile's global load and its use
+//   DIRECT_LDS       1: global-to-LDS copies without registers, NSTAGES-deep ring
+//   NSTAGES          LDS stages (2 unless DIRECT_LDS)
 //   sched(pid, &tm, &tn)
 //   a_gt(tm) a_gk(kt) a_gl(tid, u)   or   a_gf(tm, kt, tid, u)
 //   a_s(tid, u, e)                   LDS element offset of element e of load vector u
@@ -60,7 +64,7 @@ LEGO_FN mf_t lds_frag(const elem_t* base, IDX_T off) {
 
 extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restrict__ A, const elem_t* __restrict__ B,
                                                            float* __restrict__ C) {
-  __shared__ __attribute__((aligned(16))) elem_t lds[2 * STAGE];
+  __shared__ __attribute__((aligned(16))) elem_t lds[NSTAGES * STAGE];
   const IDX_T tid = threadIdx.x;
   const IDX_T lane = tid % 64u;
   const IDX_T w = tid / 64u;
@@ -80,101 +84,256 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   for (int u = 0; u < B_NV; ++u) b_loc[u] = b_gl(tid, u);
 #endif
 
-  av_t ra[A_NV];
-  bv_t rb[B_NV];
+  // Global-to-LDS staging registers.  With PREFETCH == 2 there are two sets:
+  // the tile for step kt+2 is loaded while the tile for step kt+1 (loaded one
+  // step earlier) is written to LDS, hiding more than a full step of memory
+  // latency.
+  av_t ra[PREFETCH][A_NV];
+  bv_t rb[PREFETCH][B_NV];
   acc_t acc[MI][NI];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = (acc_t){};
 
-  auto gload = [&](IDX_T kt) {
+  auto gload = [&](IDX_T kt, int rbuf) {
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
       if (A_GUARD && (IDX_T)u * NT + tid >= A_NVEC) continue;
 #if A_SEP
-      ra[u] = *(const av_t*)(Ab + a_gk(kt) + a_loc[u]);
+      ra[rbuf][u] = *(const av_t*)(Ab + a_gk(kt) + a_loc[u]);
 #else
-      ra[u] = *(const av_t*)(A + a_gf(tm, kt, tid, u));
+      ra[rbuf][u] = *(const av_t*)(A + a_gf(tm, kt, tid, u));
 #endif
     }
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
       if (B_GUARD && (IDX_T)u * NT + tid >= B_NVEC) continue;
 #if B_SEP
-      rb[u] = *(const bv_t*)(Bb + b_gk(kt) + b_loc[u]);
+      rb[rbuf][u] = *(const bv_t*)(Bb + b_gk(kt) + b_loc[u]);
 #else
-      rb[u] = *(const bv_t*)(B + b_gf(tn, kt, tid, u));
+      rb[rbuf][u] = *(const bv_t*)(B + b_gf(tn, kt, tid, u));
 #endif
     }
   };
-  auto sstore = [&](int stage) {
+  auto sstore = [&](int stage, int rbuf) {
     elem_t* la = lds + stage * STAGE;
     elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
       if (A_GUARD && (IDX_T)u * NT + tid >= A_NVEC) continue;
 #if A_SVEC
-      *(av_t*)(la + a_s(tid, u, 0)) = ra[u];
+      *(av_t*)(la + a_s(tid, u, 0)) = ra[rbuf][u];
 #else
 #pragma unroll
-      for (int e = 0; e < A_V; ++e) la[a_s(tid, u, e)] = ra[u][e];
+      for (int e = 0; e < A_V; ++e) la[a_s(tid, u, e)] = ra[rbuf][u][e];
 #endif
     }
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
       if (B_GUARD && (IDX_T)u * NT + tid >= B_NVEC) continue;
 #if B_SVEC
-      *(bv_t*)(lb + b_s(tid, u, 0)) = rb[u];
+      *(bv_t*)(lb + b_s(tid, u, 0)) = rb[rbuf][u];
 #else
 #pragma unroll
-      for (int e = 0; e < B_V; ++e) lb[b_s(tid, u, e)] = rb[u][e];
+      for (int e = 0; e < B_V; ++e) lb[b_s(tid, u, e)] = rb[rbuf][u][e];
 #endif
     }
   };
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
+  // Fragments of one k-substep, double-buffered in registers: the reads of
+  // substep s+1 are in flight while the MFMAs of substep s run.
+  mf_t af[2][MI], bf[2][NI];
+  auto fload = [&](const elem_t* la, const elem_t* lb, int s, int buf) {
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+#if A_FRVEC
+      af[buf][i] = lds_frag(la, a_fr(lane, w, i, s, 0));
+#else
+      e8_t t;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = la[a_fr(lane, w, i, s, e)];
+      af[buf][i] = __builtin_bit_cast(mf_t, t);
+#endif
+    }
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+#if B_FRVEC
+      bf[buf][j] = lds_frag(lb, b_fr(lane, w, j, s, 0));
+#else
+      e8_t t;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = lb[b_fr(lane, w, j, s, e)];
+      bf[buf][j] = __builtin_bit_cast(mf_t, t);
+#endif
+    }
+  };
 
-  for (IDX_T kt = 0; kt < KT; ++kt) {
+  // One K step on LDS stage kt&1.  `lbuf`: staging set receiving tile
+  // kt+PREFETCH; `sbuf`: staging set holding tile kt+1, written to the other
+  // LDS stage during the step.  The stage being written was last read in
+  // step kt-1, whose closing barrier retired all of its readers.
+  auto step = [&](IDX_T kt, int lbuf, int sbuf) {
     const int cur = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
+    if (kt + PREFETCH < KT) gload(kt + PREFETCH, lbuf);
+    // Keep the loads at the top: the compiler would otherwise sink them to
+    // their LDS stores.
+    __builtin_amdgcn_sched_barrier(0);
+    const elem_t* la = lds + cur * STAGE;
+    const elem_t* lb = la + A_STAGE;
+    fload(la, lb, 0, 0);
+#pragma unroll
+    for (int s = 0; s < BK / KB; ++s) {
+      if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (s == STORE_AT && kt + 1 < KT) sstore(cur ^ 1, sbuf);
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      if (s == STORE_AT) {
+        // Spread the LDS stores between the MFMAs of this substep.
+#pragma unroll
+        for (int g = 0; g < A_NV * (A_SVEC ? 1 : A_V) + B_NV * (B_SVEC ? 1 : B_V); ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // one LDS write
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+  };
+
+#if DIRECT_LDS
+  // Direct global-to-LDS copies: each lane's 16 bytes land at a wave-uniform
+  // LDS base + 16 * lane, so load vector q = u*NT + tid fills LDS slot q; the
+  // planner gave that lane the global address of the logical element the LDS
+  // layout puts in slot q (the inverse of the LDS layout drives the copy).
+  // NSTAGES LDS stages form a ring: the tile for step kt+NSTAGES-1 is
+  // requested at the top of step kt into the stage read during step kt-1.
+  const IDX_T wu = __builtin_amdgcn_readfirstlane(tid / 64u);
+  auto dload = [&](IDX_T kt, int stage) {
+    elem_t* la = lds + stage * STAGE;
+    elem_t* lb = la + A_STAGE;
+#pragma unroll
+    for (int u = 0; u < A_NV; ++u) {
+#if A_SEP
+      const elem_t* src = Ab + a_gk(kt) + a_loc[u];
+#else
+      const elem_t* src = A + a_gf(tm, kt, tid, u);
+#endif
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(la + ((IDX_T)u * NT + wu * 64u) * 8u),
+                                       16, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < B_NV; ++u) {
+#if B_SEP
+      const elem_t* src = Bb + b_gk(kt) + b_loc[u];
+#else
+      const elem_t* src = B + b_gf(tn, kt, tid, u);
+#endif
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(lb + ((IDX_T)u * NT + wu * 64u) * 8u),
+                                       16, 0, 0);
+    }
+  };
+  // s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt at their maxima).
+#define VMCNT_WAIT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | 0x70 | 0xF00)
+  // Wait until at most `after` tiles of direct loads are still in flight.
+  auto wait_tiles = [&](int after) {
+    if (after <= 0) VMCNT_WAIT(0);
+#if NSTAGES > 2
+    else if (after == 1) VMCNT_WAIT(1 * (A_NV + B_NV));
+#endif
+#if NSTAGES > 3
+    else if (after == 2) VMCNT_WAIT(2 * (A_NV + B_NV));
+#endif
+#if NSTAGES > 4
+    else VMCNT_WAIT(3 * (A_NV + B_NV));
+#endif
+  };
+#pragma unroll
+  for (int p = 0; p < NSTAGES - 1; ++p)
+    if ((IDX_T)p < KT) dload(p, p);
+  wait_tiles((int)(KT - 1 < (IDX_T)(NSTAGES - 2) ? KT - 1 : (IDX_T)(NSTAGES - 2)));
+  __syncthreads();
+  fload(lds, lds + A_STAGE, 0, 0);
+  for (IDX_T kt = 0; kt < KT; ++kt) {
+    const int cur = kt % NSTAGES;
+    // The stage receiving tile kt+NSTAGES-1 was last read before the barrier
+    // of step kt-1.
+    if (kt + NSTAGES - 1 < KT) dload(kt + NSTAGES - 1, (kt + NSTAGES - 1) % NSTAGES);
+    __builtin_amdgcn_sched_barrier(0);
     const elem_t* la = lds + cur * STAGE;
     const elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int s = 0; s < BK / KB; ++s) {
-      mf_t af[MI], bf[NI];
-#pragma unroll
-      for (int i = 0; i < MI; ++i) {
-#if A_FRVEC
-        af[i] = lds_frag(la, a_fr(lane, w, i, s, 0));
-#else
-        e8_t t;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) t[e] = la[a_fr(lane, w, i, s, e)];
-        af[i] = __builtin_bit_cast(mf_t, t);
-#endif
+      if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
+      if (s == BK / KB - 1) {
+        // Every read of this stage has been issued.  Once tile kt+1 has landed
+        // (tiles requested after it may stay in flight) and all waves are
+        // here, the first fragments of step kt+1 are fetched while the MFMAs
+        // of this last substep run.
+        const IDX_T last = (kt + NSTAGES - 1 < KT ? kt + NSTAGES - 1 : KT - 1);
+        wait_tiles(last > kt + 1 ? (int)(last - (kt + 1)) : 0);
+        __syncthreads();
+        if (kt + 1 < KT) {
+          const elem_t* na = lds + ((kt + 1) % NSTAGES) * STAGE;
+          fload(na, na + A_STAGE, 0, 0);
+        }
       }
-#pragma unroll
-      for (int j = 0; j < NI; ++j) {
-#if B_FRVEC
-        bf[j] = lds_frag(lb, b_fr(lane, w, j, s, 0));
-#else
-        e8_t t;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) t[e] = lb[b_fr(lane, w, j, s, e)];
-        bf[j] = __builtin_bit_cast(mf_t, t);
-#endif
-      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[i], bf[j], acc[i][j]);
+        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < KT) sstore(cur ^ 1);
+  }
+#elif PREFETCH == 2
+  gload(0, 0);
+  if (1 < KT) gload(1, 1);
+  sstore(0, 0);
+  __syncthreads();
+  for (IDX_T kt = 0; kt < KT; kt += 2) {
+    step(kt, 0, 1);
+    if (kt + 1 < KT) step(kt + 1, 1, 0);
+  }
+#else
+  // Single staging set: the tile for step kt+1 is loaded at the top of step
+  // kt and stored during it.
+  gload(0, 0);
+  sstore(0, 0);
+  __syncthreads();
+  for (IDX_T kt = 0; kt < KT; ++kt) {
+    if (kt + 1 < KT) gload(kt + 1, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    const int cur = kt & 1;
+    const elem_t* la = lds + cur * STAGE;
+    const elem_t* lb = la + A_STAGE;
+    fload(la, lb, 0, 0);
+#pragma unroll
+    for (int s = 0; s < BK / KB; ++s) {
+      if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (s == STORE_AT && kt + 1 < KT) sstore(cur ^ 1, 0);
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      if (s == STORE_AT) {
+#pragma unroll
+        for (int g = 0; g < A_NV * (A_SVEC ? 1 : A_V) + B_NV * (B_SVEC ? 1 : B_V); ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     __syncthreads();
   }
+#endif
 
 #if C_SEP
   float* __restrict__ Cb = C + c_t(tm, tn);

@@ -143,6 +143,17 @@ int main() {
       }
     for (char c : b) if (c != 1) FAIL("B element never loaded");
   }
+#if DIRECT_LDS
+  // direct copies: load vector q of a thread lands in LDS slot q, which the
+  // LDS layout must assign to exactly the elements that vector carries
+  for (u64 tid = 0; tid < NT; ++tid) {
+    for (u64 u = 0; u < A_NV; ++u) for (int e = 0; e < 8; ++e)
+      if ((u64)a_s((IDX_T)tid, (IDX_T)u, (IDX_T)e) != (u * NT + tid) * 8 + e) FAIL("direct A slot mismatch");
+    for (u64 u = 0; u < B_NV; ++u) for (int e = 0; e < 8; ++e)
+      if ((u64)b_s((IDX_T)tid, (IDX_T)u, (IDX_T)e) != (u * NT + tid) * 8 + e) FAIL("direct B slot mismatch");
+  }
+  if ((unsigned long long)NSTAGES * (BM + BN) * BK * 2 > 160 * 1024) FAIL("LDS ring exceeds 160 KiB");
+#endif
   // LDS stores: a bijection onto each stage
   {
     std::vector<char> la(BM * BK), lb(BN * BK);
