@@ -5,6 +5,8 @@
 // Direct path (M keeps runs of at least V elements):
 //   V, NVEC, NT, UNROLL
 //   LEGO_FN IDX_T src_vec(IDX_T t)   source vector index of destination vector t
+//   LEGO_FN IDX_T blk(IDX_T b)       destination chunk of schedule position b
+//   NBLK                             number of chunks
 // LDS path (both sides are digit permutations; a tile of TILE elements is read
 // in source order into LDS and written in destination order):
 //   TILE, NT, VL, VS, LDSW_CONTIG
@@ -12,21 +14,25 @@
 //   LEGO_FN IDX_T ldsw(IDX_T q, IDX_T e)      LDS slot of element e of that vector
 //   LEGO_FN IDX_T ldsr(IDX_T q)               LDS slot of destination-side vector q
 //   LEGO_FN IDX_T dst_off(IDX_T g, IDX_T q)   element offset of destination-side vector q
-// NONTEMPORAL selects streaming (non-temporal) global loads and stores.
+// NONTEMPORAL: bit 0 streams (non-temporal) global loads, bit 1 stores.
 
-#if NONTEMPORAL
+#if NONTEMPORAL & 1
 #define LEGO_LD(p) __builtin_nontemporal_load(p)
-#define LEGO_ST(v, p) __builtin_nontemporal_store((v), (p))
 #else
 #define LEGO_LD(p) (*(p))
+#endif
+#if NONTEMPORAL & 2
+#define LEGO_ST(v, p) __builtin_nontemporal_store((v), (p))
+#else
 #define LEGO_ST(v, p) (*(p) = (v))
 #endif
 
 #ifdef LEGO_REMAP_DIRECT
 typedef ELEM_T vec_t __attribute__((ext_vector_type(V)));
-extern "C" __global__ __launch_bounds__(NT) void lego_remap_direct(const vec_t* __restrict__ src,
-                                                                   vec_t* __restrict__ dst) {
-  const u64 base = (u64)blockIdx.x * (NT * UNROLL) + threadIdx.x;
+// Copies destination chunk c (NT*UNROLL vectors): UNROLL loads in flight per
+// thread, then UNROLL stores.
+LEGO_FN void remap_chunk(const vec_t* __restrict__ src, vec_t* __restrict__ dst, u64 c) {
+  const u64 base = c * (NT * UNROLL) + threadIdx.x;
   vec_t v[UNROLL];
 #pragma unroll
   for (int u = 0; u < UNROLL; ++u) {
@@ -38,6 +44,13 @@ extern "C" __global__ __launch_bounds__(NT) void lego_remap_direct(const vec_t* 
     const u64 t = base + (u64)u * NT;
     if (t < NVEC) LEGO_ST(v[u], dst + t);
   }
+}
+// Workgroup b handles destination chunks blk(b), blk(b + G), ... (G = the
+// grid size; NBLK chunks in all).  The chunk order is a layout chosen so that
+// the workgroups resident at one time touch spread-out source addresses.
+extern "C" __global__ __launch_bounds__(NT) void lego_remap_direct(const vec_t* __restrict__ src,
+                                                                   vec_t* __restrict__ dst) {
+  for (u64 b = blockIdx.x; b < NBLK; b += gridDim.x) remap_chunk(src, dst, (u64)blk((IDX_T)b));
 }
 #endif
 

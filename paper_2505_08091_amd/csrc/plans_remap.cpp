@@ -204,11 +204,64 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   std::ostringstream s;
   std::string info;
   bool wide = false;
-  const int nontemporal = 1;
+  // Streaming (non-temporal) loads, ordinary stores.  On MI355X this measured
+  // fastest for HBM-resident tensors that are not reused by the same kernel,
+  // both with caches cleaned between launches and when a remap consumes the
+  // previous remap's output; cached stores leave that output in the last-level
+  // cache for its consumer.
+  int nontemporal = 1;
+  if (const char* e = std::getenv("LEGO_REMAP_NONTEMPORAL")) nontemporal = std::atoi(e);
   if (R.path == REMAP_DIRECT || R.path == REMAP_GATHER) {
-    const int NT = 256, UNROLL = V >= maxv ? 4 : 8;
+    int NT = 256, UNROLL = V >= maxv ? 4 : 8;
+    if (const char* e = std::getenv("LEGO_REMAP_NT")) NT = std::atoi(e);
+    if (const char* e = std::getenv("LEGO_REMAP_UNROLL")) UNROLL = std::atoi(e);
     const i64 nvec = N / V;
-    std::string fns = emit_all({{"src_vec",
+    const i64 chunk = (i64)NT * UNROLL;
+    const i64 nblk = (nvec + chunk - 1) / chunk;
+    // Chunk order.  For a digit map whose chunks are whole digits, the
+    // workgroups enumerate the chunk digits by source weight (source order);
+    // otherwise they run in destination order.
+    std::vector<Dg> cd;  // digits of the chunk index: (dst weight in chunks, size, src weight)
+    bool src_order = pure && nvec % chunk == 0;
+    if (const char* e = std::getenv("LEGO_REMAP_ORDER")) src_order = src_order && std::string(e) != "dst";
+    if (src_order) {
+      std::vector<Dg> d;
+      for (auto& x : digits) d.push_back({x.a, x.b, x.coeff});
+      std::sort(d.begin(), d.end(), [](const Dg& x, const Dg& y) { return x.a < y.a; });
+      const i64 cel = chunk * V;  // elements per chunk
+      for (size_t k = 0; k < d.size() && src_order; ++k) {
+        if (d[k].a >= cel) {
+          if (d[k].a % cel) src_order = false;
+          cd.push_back({d[k].a / cel, d[k].b, d[k].c});
+        } else if (d[k].a * d[k].b > cel) {
+          i64 f = cel / d[k].a;
+          if (cel % d[k].a || d[k].b % f) {
+            src_order = false;
+          } else {
+            cd.push_back({1, d[k].b / f, d[k].c * f});
+          }
+        }
+      }
+      std::sort(cd.begin(), cd.end(), [](const Dg& x, const Dg& y) { return x.c < y.c; });
+    }
+    std::string fns = emit_all({{"blk",
+                                 [&](Ctx& c) {
+                                   int b = c.var("b", nblk);
+                                   Sum o = var(c, b);
+                                   if (src_order) {
+                                     o = cst(0);
+                                     i64 w = 1;
+                                     for (auto& x : cd) {
+                                       o = add(c, o, mulc(c, fmod(c, fdiv(c, var(c, b), w), x.b), x.a));
+                                       w *= x.b;
+                                     }
+                                   }
+                                   FnSpec f;
+                                   f.params = {b};
+                                   f.outs = {o};
+                                   return f;
+                                 }},
+                                {"src_vec",
                                  [&](Ctx& c) {
                                    int t = c.var("t", nvec);
                                    int pv = c.var("p", N);
@@ -220,16 +273,20 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
                                  }}},
                                &wide, &info);
     s << header() << "#define ELEM_T " << et << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define V " << V
-      << "\n#define NVEC " << nvec << "ull\n#define NT " << NT << "\n#define UNROLL " << UNROLL
+      << "\n#define NVEC " << nvec << "ull\n#define NBLK " << nblk << "ull\n#define NT " << NT << "\n#define UNROLL " << UNROLL
       << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_DIRECT 1\n"
       << fns << "// ---- template ----\n" << tpl_remap;
     R.kernel = "lego_remap_direct";
     R.block = NT;
-    R.grid = (nvec + (long long)NT * UNROLL - 1) / ((long long)NT * UNROLL);
+    // Optionally a persistent grid: `persist` workgroups per CU loop over the chunks.
+    int persist = 0;
+    if (const char* e = std::getenv("LEGO_REMAP_PERSIST")) persist = std::atoi(e);
+    R.grid = persist > 0 ? std::min<i64>(nblk, 256ll * persist) : nblk;
     R.vec = V;
     R.vec_dst = V;
     R.src = s.str();
-    R.info = std::string(R.path == REMAP_DIRECT ? "direct" : "gather") + " V=" + std::to_string(V) +
+    R.info = std::string(R.path == REMAP_DIRECT ? "direct" : "gather") + (src_order ? " src-order" : " dst-order") +
+             " NT=" + std::to_string(NT) + " UNROLL=" + std::to_string(UNROLL) + " V=" + std::to_string(V) +
              " run=" + std::to_string(run) + info;
     return R;
   }

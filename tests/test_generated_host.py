@@ -49,6 +49,14 @@ HARNESS_REMAP = r"""
 int main(int argc, char** argv) {
 #ifdef LEGO_REMAP_DIRECT
   const u64 n = NVEC * (u64)V;
+  {  // the workgroup -> chunk schedule is a bijection onto the chunks
+    const u64 chunk = (u64)NT * UNROLL, nblk = (NVEC + chunk - 1) / chunk;
+    std::vector<char> hit(nblk);
+    for (u64 b = 0; b < nblk; ++b) {
+      u64 c = (u64)blk((IDX_T)b);
+      if (c >= nblk || hit[c]++) FAIL("blk is not a bijection");
+    }
+  }
   std::vector<long long> perm(n, -1);  // dst element -> src element
   for (u64 t = 0; t < NVEC; ++t) {
     u64 s = (u64)src_vec((IDX_T)t);
