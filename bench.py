@@ -45,6 +45,29 @@ def _avg_ms(evs):
     return sum(s.elapsed_time(e) for s, e in evs) / len(evs)
 
 
+def _source_sha1(L, kind, *args, **kw):
+    import hashlib
+    return hashlib.sha1(L.plan_source(kind, *args, **kw).encode()).hexdigest()
+
+
+def profiled_traffic(name, sha1):
+    """HBM traffic per launch measured with rocprofv3 (FETCH_SIZE + WRITE_SIZE,
+    scaled by the same counters for a copy of known size), read from the
+    committed profile summary - only if it was taken on this exact generated
+    kernel source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"{name}.md")
+    try:
+        with open(path) as f:
+            for line in f:
+                if line.startswith("traffic-json:"):
+                    d = json.loads(line.split(":", 1)[1])
+                    if d.get("source_sha1") == sha1:
+                        return d["bytes_per_launch"]
+    except OSError:
+        pass
+    return None
+
+
 def bench_remap(L, steps, warmup):
     import torch
     import synth_inputs as S
@@ -86,6 +109,7 @@ def bench_remap(L, steps, warmup):
         e.record()
     torch.cuda.synchronize()
     return {
+        "sha1": _source_sha1(L, "remap", row, blk, param=4),
         "total_ms": total_ms,
         "launch_ms": _avg_ms(evs),
         "fwd_ms": _avg_ms(evs[0::2]),
@@ -117,7 +141,8 @@ def bench_gemm(L, steps, warmup):
     ms = _avg_ms(evs)
     flops = 2.0 * n ** 3
     tf = flops / (ms * 1e-3) / 1e12
-    return {"ms": ms, "tflops": tf, "plan": plan, "a": a, "b": b, "c": c}
+    return {"ms": ms, "tflops": tf, "plan": plan, "a": a, "b": b, "c": c,
+            "sha1": _source_sha1(L, "gemm", M=n, N=n, K=n, dtype="bf16")}
 
 
 def cpu_baseline_remap():
@@ -201,7 +226,8 @@ def main():
             "identity_copy_GBps": round(r["bytes_per_launch"] / (r["copy_ms"] * 1e-3) / 1e9, 1),
         },
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": profiled_traffic("remap_direct_8192x8192_f32_row_to_blocked", r["sha1"]),
                      "kernel": "lego_remap_direct", "bytes_per_launch": r["bytes_per_launch"],
                      "avg_launch_ms": round(r["launch_ms"], 5)},
     }
@@ -213,7 +239,8 @@ def main():
                         "256x256x64 tiles, grouped (8) + XCD schedule, XOR-swizzled LDS",
             "plan": g["plan"], "steps": args.gemm_steps,
             "roofline": {"bound": "mfma", "achieved": round(g["tflops"], 1), "peak": BF16_PEAK_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(g["tflops"] / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                         "unit": "TFLOP/s", "frac": round(g["tflops"] / BF16_PEAK_TFLOPS, 4),
+                         "traffic": profiled_traffic("gemm_8192_bf16", g["sha1"]),
                          "kernel": "lego_gemm", "flops_per_launch": 2 * N_GEMM ** 3,
                          "avg_launch_ms": round(g["ms"], 5)},
         }

@@ -144,6 +144,9 @@ class Piece(_Handle):
 
 
 def RegP(dims, sigma):  # noqa: N802 (paper notation)
+    if len(sigma) != len(dims):
+        # the C call reads len(dims) permutation entries
+        raise LegoError(-1, "sigma must have one entry per tile dimension")
     out = ctypes.c_void_p()
     s = (ctypes.c_int32 * len(sigma))(*[int(x) for x in sigma])
     _check(_lib.lego_regp(len(dims), _i64(dims), s, ctypes.byref(out)))
@@ -203,6 +206,8 @@ class Layout(_Handle):
         return n.value
 
     def apply(self, idx):
+        if len(idx) != self.rank():
+            raise LegoError(-1, "index rank differs from the layout rank")
         f = ctypes.c_int64()
         _check(_lib.lego_apply(self.h, _i64(idx), ctypes.byref(f)))
         return f.value
@@ -235,6 +240,8 @@ def GroupBy(*tiles):  # noqa: N802
 
 def TileBy(*tiles):  # noqa: N802
     q, d = len(tiles), len(tiles[0])
+    if any(len(t) != d for t in tiles):
+        raise LegoError(-1, "TileBy levels must have equal rank")
     flat = [int(x) for t in tiles for x in t]
     out = ctypes.c_void_p()
     _check(_lib.lego_tileby(q, d, _i64(flat), ctypes.byref(out)))
@@ -255,6 +262,8 @@ def as_layout(piece):
 
 
 def ExpandBy(n, n_expanded, g):  # noqa: N802
+    if len(n) != len(n_expanded):
+        raise LegoError(-1, "ExpandBy extents must have equal rank")
     out = ctypes.c_void_p()
     _check(_lib.lego_expandby(len(n), _i64(n), _i64(n_expanded), g.h, ctypes.byref(out)))
     return Layout(out)

@@ -1,0 +1,156 @@
+"""C ABI checks that need no GPU: exported symbols, error codes, host
+evaluation of layouts against the oracle, lowering output."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import layout as OL
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "lego.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lego_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lego):
+    lib = ctypes.CDLL(lego.library_path())
+    names = _declared()
+    assert len(names) >= 30
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    # and the binding exposes the same names
+    assert set(names) <= set(lego.EXPORTED)
+
+
+def test_version_and_last_error(lego):
+    assert b"gfx950" in lego.lego_version()
+    with pytest.raises(lego.LegoError):
+        lego.RegP([2, 2], [1, 1])
+    assert lego.lego_last_error()
+
+
+@pytest.mark.parametrize("call,status", [
+    (lambda L: L.RegP([2, 3], [1, 1]), "NOT_PERMUTATION"),
+    (lambda L: L.RegP([2, 0], [1, 2]), "INVALID_ARG"),
+    (lambda L: L.RegP([2, 3], [1]), "INVALID_ARG"),
+    (lambda L: L.GroupBy([4, 4]).OrderBy(L.Row(3, 5)), "SIZE_MISMATCH"),
+    (lambda L: L.GenP("morton", [6, 8]), "INVALID_ARG"),
+    (lambda L: L.GenP("xor_swizzle", [8, 24], [8, 1]), "INVALID_ARG"),
+    (lambda L: L.GenP("antidiag", [3, 4]), "INVALID_ARG"),
+    (lambda L: L.GenP(99, [3, 3]), "INVALID_ARG"),
+    (lambda L: L.as_layout(L.Row(4, 4)).apply([4, 0]), "OUT_OF_RANGE"),
+    (lambda L: L.as_layout(L.Row(4, 4)).inv(16), "OUT_OF_RANGE"),
+    (lambda L: L.ExpandBy([5, 7], [6, 9], L.TileOrderBy(L.Row(3, 2), L.Row(2, 4))), "SIZE_MISMATCH"),
+    (lambda L: L.gemm_plan(100, 64, 64, "f16"), "UNSUPPORTED"),
+    (lambda L: L.gemm_plan(64, 64, 64, "f32"), "INVALID_ARG"),
+    (lambda L: L.gemm_plan(256, 256, 256, "f16", a=L.as_layout(L.Row(128, 256))), "SIZE_MISMATCH"),
+    (lambda L: L.remap_plan(L.as_layout(L.Row(4, 4)), L.as_layout(L.Row(2, 8)), 4), "SIZE_MISMATCH"),
+    (lambda L: L.remap_plan(L.as_layout(L.Row(4, 4)), L.as_layout(L.Row(4, 4)), 3), "INVALID_ARG"),
+    (lambda L: L.remap_plan(L.ExpandBy([3, 3], [4, 4], L.as_layout(L.Row(4, 4))),
+                            L.ExpandBy([3, 3], [4, 4], L.as_layout(L.Row(4, 4))), 4), "UNSUPPORTED"),
+    (lambda L: L.mfma_fragment_layout(7, 0), "INVALID_ARG"),
+])
+def test_error_codes(lego, call, status):
+    with pytest.raises(lego.LegoError) as e:
+        call(lego)
+    assert e.value.status == status
+
+
+def test_null_pointers_rejected(lego):
+    out = ctypes.c_void_p()
+    assert lego.lego_regp(2, None, None, ctypes.byref(out)) == -1
+    assert lego.lego_apply(None, None, None) == -1
+    assert lego.lego_remap(None, None, 4, None, None, None) == -1
+    lego.lego_release(None)  # ignored
+
+
+def _pairs(L):
+    return [
+        (L.GroupBy([6, 4]).OrderBy(L.RegP([2, 2], [2, 1]), L.GenP("reverse", [3, 2])),
+         OL.GroupBy([6, 4], chain=[OL.OrderBy(OL.RegP([2, 2], [2, 1]), OL.reverse_genp(3, 2))])),
+        (L.GroupBy([6, 6]).OrderBy(L.RegP([2, 3, 2, 3], [1, 3, 2, 4])).OrderBy(L.RegP([2, 2], [2, 1]),
+                                                                             L.GenP("antidiag", [3, 3])),
+         OL.GroupBy([6, 6]).OrderBy(OL.RegP([2, 3, 2, 3], [1, 3, 2, 4])).OrderBy(OL.RegP([2, 2], [2, 1]),
+                                                                               OL.antidiag_genp(3))),
+        (L.TileBy([3, 4], [2, 5]), OL.TileBy([3, 4], [2, 5])),
+        (L.TileOrderBy(L.Col(3, 5), L.Row(7, 3)), OL.TileOrderBy(OL.Col(3, 5), OL.Row(7, 3))),
+        (L.as_layout(L.GenP("morton", [16, 8])), OL.as_layout(OL.morton_genp(16, 8))),
+        (L.as_layout(L.GenP("xor_swizzle", [32, 32], [4, 2])), OL.as_layout(OL.xor_swizzle_genp(32, 32, 4, 2))),
+        (L.as_layout(L.GenP("antidiag", [9, 9])), OL.as_layout(OL.antidiag_genp(9))),
+        (L.GroupBy([2, 2, 2, 2, 2]).OrderBy(L.RegP([2] * 5, [5, 2, 4, 3, 1])),
+         OL.GroupBy([2, 2, 2, 2, 2]).OrderBy(OL.RegP([2] * 5, [5, 2, 4, 3, 1]))),
+        (L.GroupBy([3, 3], [4, 4]).OrderBy(L.Row(12, 12)), OL.GroupBy([3, 3], [4, 4]).OrderBy(OL.Row(12, 12))),
+        (L.GroupBy([12, 20]).OrderBy(L.RegP([3, 4, 4, 5], [2, 4, 1, 3])).OrderBy(L.Col(16, 15))
+         .OrderBy(L.GenP("reverse", [10, 24])),
+         OL.GroupBy([12, 20]).OrderBy(OL.RegP([3, 4, 4, 5], [2, 4, 1, 3])).OrderBy(OL.Col(16, 15))
+         .OrderBy(OL.reverse_genp(10, 24))),
+        (L.ExpandBy([5, 7], [6, 8], L.TileOrderBy(L.Row(3, 2), L.Row(2, 4))),
+         OL.ExpandBy([5, 7], [6, 8], OL.TileOrderBy(OL.Row(3, 2), OL.Row(2, 4)))),
+    ]
+
+
+def test_host_apply_inv_match_oracle(lego):
+    for lay, olay in _pairs(lego):
+        dims = lay.dims()
+        assert dims == list(olay.dims())
+        n = int(np.prod(dims))
+        for x in range(n):
+            idx = OL.canon_unflatten(dims, x)
+            f = lay.apply(idx)
+            assert f == int(olay.apply(idx))
+            if f >= 0:
+                assert lay.inv(f) == [int(v) for v in olay.inv(f)]
+
+
+def test_verify_bijective(lego):
+    for lay, _ in _pairs(lego):
+        assert lay.verify_bijective()
+    with pytest.raises(lego.LegoError) as e:
+        lego.as_layout(lego.Row(8192, 8192)).verify_bijective(max_points=1000)
+    assert e.value.status == "INVALID_ARG"
+
+
+def test_emit_shows_closed_form_and_op_counts(lego):
+    txt = lego.TileOrderBy(lego.Col(128, 128), lego.Row(64, 64)).emit("apply")
+    assert "ops: 8" in txt and "u32" in txt and "/" not in txt.split("\n", 1)[1].replace("//", "")
+    txt = lego.as_layout(lego.GenP("antidiag", [6, 6])).emit("inv")
+    assert "lego_isqrt" in txt
+
+
+def test_fragment_layouts_match_isa_formulas(lego):
+    fa = lego.mfma_fragment_layout(0, 0)
+    fc = lego.mfma_fragment_layout(0, 2)
+    for lane in range(64):
+        for e in range(8):
+            assert fa.apply([lane, e]) == (lane % 32) * 16 + 8 * (lane // 32) + e
+        for r in range(16):
+            row, col = divmod(fc.apply([lane, r]), 32)
+            assert (row, col) == (8 * (r // 4) + 4 * (lane // 32) + r % 4, lane % 32)
+    fa16 = lego.mfma_fragment_layout(1, 0)
+    fc16 = lego.mfma_fragment_layout(1, 2)
+    for lane in range(64):
+        for e in range(8):
+            assert fa16.apply([lane, e]) == (lane % 16) * 32 + 8 * (lane // 16) + e
+        for r in range(4):
+            assert divmod(fc16.apply([lane, r]), 16) == (4 * (lane // 16) + r, lane % 16)
+
+
+def test_plans_choose_expected_paths(lego):
+    L = lego
+    row = L.as_layout(L.Row(8192, 8192))
+    blk = L.TileOrderBy(L.Col(128, 128), L.Row(64, 64))
+    p = L.remap_plan(row, blk, 4)
+    assert p["path"] == "direct" and p["run"] == 64 and p["vec"] == 4
+    mz = L.as_layout(L.GenP("morton", [4096, 4096]))
+    p = L.remap_plan(L.as_layout(L.Row(4096, 4096)), mz, 2)
+    assert p["path"] == "lds" and p["vec"] == 8
+    p = L.remap_plan(L.as_layout(L.Row(6, 6)), L.as_layout(L.GenP("antidiag", [6, 6])), 4)
+    assert p["path"] == "gather"
+    info = L.gemm_plan(8192, 8192, 8192, "bf16")
+    assert "direct-lds" in info and "A:V8k sep" in info and "frvec" in info
