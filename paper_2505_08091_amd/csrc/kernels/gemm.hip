@@ -269,7 +269,6 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     const elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int s = 0; s < BK / KB; ++s) {
-      if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
       if (s == BK / KB - 1) {
         // Every read of this stage has been issued.  Once tile kt+1 has landed
         // (tiles requested after it may stay in flight) and all waves are
@@ -278,16 +277,28 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         const IDX_T last = (kt + NSTAGES - 1 < KT ? kt + NSTAGES - 1 : KT - 1);
         wait_tiles(last > kt + 1 ? (int)(last - (kt + 1)) : 0);
         __syncthreads();
-        if (kt + 1 < KT) {
-          const elem_t* na = lds + ((kt + 1) % NSTAGES) * STAGE;
-          fload(na, na + A_STAGE, 0, 0);
-        }
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      // Fragments of the next substep are read between these MFMAs, never
+      // ahead of them: with direct loads in flight the only wait the compiler
+      // can place before an MFMA is one for every outstanding LDS read, so a
+      // read issued before this block would stall it.
+      if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
+      else if (kt + 1 < KT) {
+        const elem_t* na = lds + ((kt + 1) % NSTAGES) * STAGE;
+        fload(na, na + A_STAGE, 0, 0);
+      }
+#pragma unroll
+      for (int g = 0; g < (MI + NI < MI * NI ? MI + NI : MI * NI); ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, MI * NI, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
