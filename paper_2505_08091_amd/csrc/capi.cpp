@@ -109,9 +109,23 @@ void hip_check(hipError_t e, const char* what) {
 }
 
 void launch(const KernelPlan& k, void** args, void* stream) {
-  JitKernel jk = jit_get(k.src, k.kernel);
   if (k.grid <= 0 || k.grid > 0x7fffffffll) throw Unsupported("grid too large");
-  hip_check(hipModuleLaunchKernel(jk.fn, (unsigned)k.grid, 1, 1, (unsigned)k.block, 1, 1, 0, (hipStream_t)stream,
+  int dev = 0;
+  hip_check(hipGetDevice(&dev), "hipGetDevice");
+  const bool slot = dev >= 0 && dev < FnCache::kDevices;
+  hipFunction_t fn = nullptr;
+  if (slot) {
+    std::lock_guard<std::mutex> lk(k.fns.mu);
+    fn = (hipFunction_t)k.fns.fn[dev];
+  }
+  if (!fn) {
+    fn = jit_get(k.src, k.kernel).fn;
+    if (slot) {
+      std::lock_guard<std::mutex> lk(k.fns.mu);
+      k.fns.fn[dev] = (void*)fn;
+    }
+  }
+  hip_check(hipModuleLaunchKernel(fn, (unsigned)k.grid, 1, 1, (unsigned)k.block, 1, 1, 0, (hipStream_t)stream,
                                   args, nullptr),
             "hipModuleLaunchKernel");
 }

@@ -3,6 +3,7 @@
 // source for gfx950); launching does.
 #pragma once
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -10,12 +11,29 @@
 
 namespace lego {
 
+// Loaded kernel functions of one plan object, per device ordinal, so that a
+// launch of a cached plan skips hashing its source.  A copy starts empty: the
+// copy may be edited into a different source.
+struct FnCache {
+  static constexpr int kDevices = 64;
+  FnCache() = default;
+  FnCache(const FnCache&) {}
+  FnCache& operator=(const FnCache&) {
+    std::lock_guard<std::mutex> lk(mu);
+    for (auto& f : fn) f = nullptr;
+    return *this;
+  }
+  mutable std::mutex mu;
+  mutable void* fn[kDevices] = {};
+};
+
 struct KernelPlan {
   std::string src;      // complete generated HIP source
   std::string kernel;   // extern "C" kernel name
   long long grid = 1;   // workgroups (1D)
   int block = 256;      // threads per workgroup
   std::string info;     // human-readable summary (path, vector widths, op counts)
+  FnCache fns;          // filled by the first launch on each device
 };
 
 // Index-map evaluation over all points: which = 0 apply (logical flat order),
