@@ -332,14 +332,17 @@ def selftest_compile():
     return n.value, info.value.decode()
 
 
-def plan_source(kind, a=None, b=None, param=0, **gemm_kw):
-    """Generated source of a plan: kind 'apply'/'inv' (param = idx_bytes),
-    'remap' (param = elem_bytes) or 'gemm' (gemm_kw as for gemm())."""
+def plan_source(kind, x=None, y=None, param=0, **gemm_kw):
+    """Generated source of a plan: kind 'apply'/'inv' of layout x (param =
+    idx_bytes), 'remap' from layout x to layout y (param = elem_bytes) or
+    'gemm' (gemm_kw as for gemm(), operand layouts included)."""
     k = {"apply": 0, "inv": 1, "remap": 2, "gemm": 3}[kind]
+    if k != 3 and gemm_kw:
+        raise TypeError(f"unexpected arguments for '{kind}': {sorted(gemm_kw)}")
     d = ctypes.byref(_desc(**gemm_kw)) if k == 3 else None
     need = ctypes.c_size_t()
-    ah = a.h if a is not None else None
-    bh = b.h if b is not None else None
+    ah = x.h if x is not None else None
+    bh = y.h if y is not None else None
     _check(_lib.lego_plan_source(k, ah, bh, int(param), d, None, 0, ctypes.byref(need)))
     buf = ctypes.create_string_buffer(need.value)
     _check(_lib.lego_plan_source(k, ah, bh, int(param), d, buf, need.value, ctypes.byref(need)))

@@ -68,6 +68,20 @@ LayoutP default_lds(i64 rows, i64 k) {
   return make_from_piece(make_row({rows, k}));
 }
 
+// LDS tile for an operand that is contiguous along m (A) or n (B) in global
+// memory: stored one k-row at a time with the m/n index fastest, so global
+// vectors land unchanged, and 64-byte granules of a k-row XOR-permuted by the
+// k-row (a GenP over [k, rows]).  Fragments are read with the transposing LDS
+// load, which fetches 4 consecutive m/n elements per lane from 4 k-rows: the
+// 4 k-rows of one read then fall in 4 distinct granules of a 256-byte bank
+// window.
+LayoutP tr_lds(i64 rows, i64 k) {
+  LayoutP base = make_orderby(make_groupby({rows, k}), {make_regp({rows, k}, {2, 1})});
+  if (rows % 32 == 0 && pow2(rows / 32) && rows / 32 >= 2)
+    return make_orderby(base, {make_genp(GEN_XOR_SWIZZLE, {k, rows}, {32, 1})});
+  return base;
+}
+
 void need_dims(const LayoutP& l, std::vector<i64> d, const char* what) {
   if (l->dims() != d) throw std::length_error(std::string(what) + " layout has the wrong logical shape");
   if (l->expand_inner) throw Unsupported(std::string(what) + ": ExpandBy layouts are not supported by the GEMM");
@@ -95,8 +109,11 @@ struct Operand {
   LayoutP glob, lds;
   bool is_b;
   int V = 1, axis = 1, NV = 1;
+  int gaxis = 1;  // axis of the widest contiguous global vector (reported)
   i64 NVEC = 0;
   bool guard = false, sep = false, svec = false, frvec = false;
+  bool frtr = false;      // fragments read with the transposing LDS load
+  bool user_lds = false;  // LDS layout given by the caller
   bool direct = false;  // load vector q fills LDS slot q (direct global-to-LDS copy)
 };
 
@@ -155,6 +172,8 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   LayoutP FC = mfma_fragment_layout(MB == 32 ? 0 : 1, 2);
 
   Operand ops[2] = {{bm, bk, LA, SA, false}, {bn, bk, LB, SB, true}};
+  ops[0].user_lds = (bool)rq.lds_a;
+  ops[1].user_lds = (bool)rq.lds_b;
   // With a single round of load vectors, only threads below NVEC load; giving
   // tid that range lets the range analysis prove separability.
   auto tid_ext = [&](const Operand& o) -> i64 { return o.NV == 1 ? std::min<i64>(NT, o.NVEC) : NT; };
@@ -213,6 +232,9 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       }
       if (found) break;
     }
+    o.gaxis = o.axis;
+    // An operand contiguous along m/n keeps that orientation in LDS.
+    if (!o.user_lds && o.axis == 0 && o.V >= 4) o.lds = tr_lds(o.R, o.KD);
     o.NVEC = o.R * o.KD / o.V;
     o.NV = (int)((o.NVEC + NT - 1) / NT);
     o.guard = o.NVEC % NT != 0;
@@ -249,6 +271,30 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
       Sum kk = add(c, mulc(c, var(c, s), KB), k);
       o.frvec = contiguous_in(o.lds->apply(al, {row, kk}), e, 8);
+    }
+    // Transposing fragment read (ds_read_b64_tr_b16): in each 16-lane block b,
+    // lane i receives element j from the address of lane 16b + 4j + i/4 plus
+    // i%4.  It serves a fragment when 4 lanes 4q..4q+3 of a block hold 4
+    // consecutive rows at equal k (checked on the fragment layout) and 4
+    // consecutive rows are 4 contiguous LDS elements, 4-aligned (checked on
+    // the LDS layout).
+    if (!o.frvec) {
+      IntAlg ia;
+      bool lanes_ok = true;
+      for (i64 l0 = 0; l0 < 64 && lanes_ok; l0 += 4)
+        for (i64 e = 0; e < 8 && lanes_ok; ++e) {
+          i64 f0 = FA->apply(ia, {l0, e});
+          for (i64 t = 1; t < 4; ++t)
+            if (FA->apply(ia, {l0 + t, e}) != f0 + t * KB) lanes_ok = false;
+        }
+      Ctx c;
+      int w = c.var("w", NWAVES), mi = c.var("mi", o.is_b ? NI : MI), rr = c.var("rr", MB / 4),
+          kq = c.var("kq", bk), t = c.var("t", 4);
+      SymAlg al{&c};
+      Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)),
+                    add(c, mulc(c, var(c, rr), 4), var(c, t)));
+      o.frtr = lanes_ok && contiguous_in(o.lds->apply(al, {row, var(c, kq)}), t, 4);
     }
   }
 
@@ -397,6 +443,27 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
                      f.outs = {oo.lds->apply(al, {row, kk})};
                      return f;
                    }});
+    if (o.frtr)
+      fns.push_back({p + "ft", [&, k](Ctx& c) {
+                       // Address lane `lane` supplies to the transposing read of
+                       // half h: the element that lane 16*(lane/16) + 4*(lane%4)
+                       // needs at fragment element 4h + (lane%16)/4.
+                       const Operand& oo = ops[k];
+                       int lane = c.var("lane", 64), w = c.var("w", NWAVES), mi = c.var("mi", oo.is_b ? NI : MI),
+                           s = c.var("s", bk / KB), h = c.var("h", 2);
+                       SymAlg al{&c};
+                       Sum lp = add(c, mulc(c, fdiv(c, var(c, lane), 16), 16), mulc(c, fmod(c, var(c, lane), 4), 4));
+                       Sum ep = add(c, mulc(c, var(c, h), 4), fdiv(c, fmod(c, var(c, lane), 16), 4));
+                       Sum f0 = FA->apply(al, {lp, ep});
+                       Sum r = fdiv(c, f0, KB), kq = fmod(c, f0, KB);
+                       Sum wpos = oo.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+                       Sum row = add(c, add(c, mulc(c, wpos, oo.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+                       Sum kk = add(c, mulc(c, var(c, s), KB), kq);
+                       FnSpec f;
+                       f.params = {lane, w, mi, s, h};
+                       f.outs = {oo.lds->apply(al, {row, kk})};
+                       return f;
+                     }});
   }
   auto c_full = [&](Ctx& c, int* tm, int* tn, int* lane, int* w, int* mi, int* ni, int* r) {
     *tm = c.var("tm", Mt);
@@ -474,7 +541,8 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
     const Operand& o = ops[k];
     s << "#define " << P2[k] << "NV " << o.NV << "\n#define " << P2[k] << "V " << o.V << "\n#define " << P2[k]
       << "SEP " << (o.sep ? 1 : 0) << "\n#define " << P2[k] << "SVEC " << (o.svec ? 1 : 0) << "\n#define " << P2[k]
-      << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "NVEC " << o.NVEC << "u\n#define " << P2[k]
+      << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "FRTR " << (o.frtr ? 1 : 0) << "\n#define " << P2[k]
+      << "NVEC " << o.NVEC << "u\n#define " << P2[k]
       << "GUARD " << (o.guard ? 1 : 0) << "\n";
   }
   // Two staging register sets when the accumulators live in AGPRs (one wave
@@ -498,11 +566,11 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   std::ostringstream info;
   info << "gemm " << M << "x" << N << "x" << K << (rq.dtype == LEGO_BF16 ? " bf16" : " f16") << " tile " << bm << "x"
        << bn << "x" << bk << " waves " << NWM << "x" << NWN << " wave " << wm << "x" << wn << " mfma " << MB << "x"
-       << MB << "x" << KB << " sched" << (xcd ? "+xcd" : "") << " A:V" << ops[0].V << (ops[0].axis ? "k" : "m")
+       << MB << "x" << KB << " sched" << (xcd ? "+xcd" : "") << " A:V" << ops[0].V << (ops[0].gaxis ? "k" : "m")
        << (ops[0].sep ? " sep" : " full") << (ops[0].svec ? " svec" : " sscalar")
-       << (ops[0].frvec ? " frvec" : " frscalar") << " B:V" << ops[1].V << (ops[1].axis ? "k" : "n")
-       << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
-       << (ops[1].frvec ? " frvec" : " frscalar") << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
+       << (ops[0].frvec ? " frvec" : (ops[0].frtr ? " frtr" : " frscalar")) << " B:V" << ops[1].V
+       << (ops[1].gaxis ? "k" : "n") << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
+       << (ops[1].frvec ? " frvec" : (ops[1].frtr ? " frtr" : " frscalar")) << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
        << (direct ? " direct-lds" : " staged") << " stages " << nstages << " lds " << nstages * stage_bytes
        << "B ops" << opsinfo.str();
   g.info = info.str();

@@ -24,6 +24,8 @@
 //   a_gt(tm) a_gk(kt) a_gl(tid, u)   or   a_gf(tm, kt, tid, u)
 //   a_s(tid, u, e)                   LDS element offset of element e of load vector u
 //   a_fr(lane, w, mi, s, e)          LDS element offset of fragment element e
+//   A_FRTR, a_ft(lane, w, mi, s, h)  fragments read with the transposing LDS
+//                                    load: the address lane supplies for half h
 //   (b_* likewise with tn)
 //   c_t(tm, tn) c_l(lane, w, mi, ni, r)   or   c_f(tm, tn, lane, w, mi, ni, r)
 
@@ -61,6 +63,45 @@ typedef float acc_t __attribute__((ext_vector_type(4)));
 LEGO_FN mf_t lds_frag(const elem_t* base, IDX_T off) {
   return __builtin_bit_cast(mf_t, *(const e8_t*)(base + off));
 }
+
+// Fragment through two transposing LDS loads (ds_read_b64_tr_b16): elements
+// 0-3 from the addresses of half 0, elements 4-7 from those of half 1.  The
+// loads are issued as inline assembly: the compiler's own form of this load is
+// ordered behind every direct global-to-LDS copy in flight (a full vmcnt wait
+// before each read), which would serialize the copies with the MFMAs.  The
+// compiler does not track these loads, so FRAG_WAIT below waits for them
+// before their fragments are used and before every barrier.
+typedef short s4_t __attribute__((ext_vector_type(4)));
+LEGO_FN s4_t lds_read_tr(const elem_t* p) {
+  s4_t r;
+  const unsigned a = (unsigned)(unsigned long)(__attribute__((address_space(3))) const void*)p;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(a));
+  return r;
+}
+LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
+  const s4_t lo = lds_read_tr(base + off0);
+  const s4_t hi = lds_read_tr(base + off1);
+  const e8_t t = {(elem_t)lo[0], (elem_t)lo[1], (elem_t)lo[2], (elem_t)lo[3],
+                  (elem_t)hi[0], (elem_t)hi[1], (elem_t)hi[2], (elem_t)hi[3]};
+  return __builtin_bit_cast(mf_t, t);
+}
+#if A_FRTR || B_FRTR
+// s_waitcnt lgkmcnt(0) (vmcnt and expcnt at their maxima), then no motion
+// across it.
+#define FRAG_WAIT()                         \
+  do {                                      \
+    __builtin_amdgcn_s_waitcnt(0xC07F);     \
+    __builtin_amdgcn_sched_barrier(0);      \
+  } while (0)
+#else
+#define FRAG_WAIT() \
+  do {              \
+  } while (0)
+#endif
+// LDS read instructions per fragment.
+#define A_FRD (A_FRTR ? 2 : (A_FRVEC ? 1 : 8))
+#define B_FRD (B_FRTR ? 2 : (B_FRVEC ? 1 : 8))
+#define FRAG_READS (MI * A_FRD + NI * B_FRD)
 
 extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restrict__ A, const elem_t* __restrict__ B,
                                                            float* __restrict__ C) {
@@ -147,7 +188,9 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   auto fload = [&](const elem_t* la, const elem_t* lb, int s, int buf) {
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
-#if A_FRVEC
+#if A_FRTR
+      af[buf][i] = lds_frag_tr(la, a_ft(lane, w, i, s, 0), a_ft(lane, w, i, s, 1));
+#elif A_FRVEC
       af[buf][i] = lds_frag(la, a_fr(lane, w, i, s, 0));
 #else
       e8_t t;
@@ -158,7 +201,9 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     }
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
-#if B_FRVEC
+#if B_FRTR
+      bf[buf][j] = lds_frag_tr(lb, b_ft(lane, w, j, s, 0), b_ft(lane, w, j, s, 1));
+#elif B_FRVEC
       bf[buf][j] = lds_frag(lb, b_fr(lane, w, j, s, 0));
 #else
       e8_t t;
@@ -184,6 +229,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     fload(la, lb, 0, 0);
 #pragma unroll
     for (int s = 0; s < BK / KB; ++s) {
+      FRAG_WAIT();
       if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);
       if (s == STORE_AT && kt + 1 < KT) sstore(cur ^ 1, sbuf);
@@ -269,6 +315,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     const elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int s = 0; s < BK / KB; ++s) {
+      FRAG_WAIT();
       if (s == BK / KB - 1) {
         // Every read of this stage has been issued.  Once tile kt+1 has landed
         // (tiles requested after it may stay in flight) and all waves are
@@ -293,12 +340,12 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         fload(na, na + A_STAGE, 0, 0);
       }
 #pragma unroll
-      for (int g = 0; g < (MI + NI < MI * NI ? MI + NI : MI * NI); ++g) {
+      for (int g = 0; g < (FRAG_READS < MI * NI ? FRAG_READS : MI * NI); ++g) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
       }
       __builtin_amdgcn_sched_group_barrier(0x008, MI * NI, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, FRAG_READS, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -326,6 +373,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     fload(la, lb, 0, 0);
 #pragma unroll
     for (int s = 0; s < BK / KB; ++s) {
+      FRAG_WAIT();
       if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);
       if (s == STORE_AT && kt + 1 < KT) sstore(cur ^ 1, 0);

@@ -191,6 +191,29 @@ int main() {
     for (int c : rb) nb += c != 0;
     if (na != (long long)MI * MB * BK || nb != (long long)NI * MB * BK) FAIL("fragments do not cover the wave tile");
   }
+  // transposing fragment reads: lane i of 16-lane block b receives element j
+  // of half h from the address of lane 16b + 4j + i/4, plus i%4; that must be
+  // the element the fragment layout gives (lane, 4h + j)
+#if A_FRTR || B_FRTR
+  for (u64 w = 0; w < NWAVES; ++w)
+    for (u64 s = 0; s < BK / KB; ++s) for (u64 h = 0; h < 2; ++h) for (u64 l = 0; l < 64; ++l) for (u64 j = 0; j < 4; ++j) {
+      u64 sup = 16 * (l / 16) + 4 * j + (l % 16) / 4;
+#if A_FRTR
+      for (u64 mi = 0; mi < MI; ++mi) {
+        u64 o = a_ft((IDX_T)sup, (IDX_T)w, (IDX_T)mi, (IDX_T)s, (IDX_T)h);
+        if (o % 4 || o + 4 > BM * BK) FAIL("a_ft misaligned or out of range");
+        if (o + l % 4 != (u64)a_fr((IDX_T)l, (IDX_T)w, (IDX_T)mi, (IDX_T)s, (IDX_T)(4 * h + j))) FAIL("a_ft mismatch");
+      }
+#endif
+#if B_FRTR
+      for (u64 ni = 0; ni < NI; ++ni) {
+        u64 o = b_ft((IDX_T)sup, (IDX_T)w, (IDX_T)ni, (IDX_T)s, (IDX_T)h);
+        if (o % 4 || o + 4 > BN * BK) FAIL("b_ft misaligned or out of range");
+        if (o + l % 4 != (u64)b_fr((IDX_T)l, (IDX_T)w, (IDX_T)ni, (IDX_T)s, (IDX_T)(4 * h + j))) FAIL("b_ft mismatch");
+      }
+#endif
+    }
+#endif
   // epilogue: every C element written exactly once
   {
     std::vector<char> c(GEMM_M * GEMM_N);
@@ -345,10 +368,13 @@ def _gemm_cases():
     cases.append(dict(M=4096, N=4096, K=4096, dtype="f16", a=L.as_layout(L.GenP("morton", [4096, 4096])),
                       b=L.as_layout(L.Row(4096, 4096))))
     cases.append(dict(M=256, N=256, K=256, dtype="f16", bm=128, bn=128, bk=32, wm=64, wn=64))  # smoke
+    for la, lb in (("Row", "Row"), ("Col", "Row"), ("Col", "Col")):  # m/n-contiguous operands, default plan
+        cases.append(dict(M=2048, N=2048, K=2048, dtype="f16", a=L.as_layout(getattr(L, la)(2048, 2048)),
+                          b=L.as_layout(getattr(L, lb)(2048, 2048))))
     return cases
 
 
-@pytest.mark.parametrize("i", range(14))
+@pytest.mark.parametrize("i", range(16))
 def test_gemm_sources_of_gpu_cases(i):
     import paper_2505_08091_amd as L
     cases = _gemm_cases()

@@ -155,3 +155,22 @@ def test_gemm_errors(lego):
     with pytest.raises(lego.LegoError) as e:
         lego.gemm(a, a, c, 64, 64, 64, "f32")
     assert e.value.status == "INVALID_ARG"
+
+
+@pytest.mark.parametrize("la_name,lb_name", [("Row", "Row"), ("Col", "Row"), ("Col", "Col")])
+def test_gemm_mn_contiguous_operands_2048(lego, la_name, lb_name):
+    """2048^3 fp16 with the default 256x256x64 plan for operands contiguous
+    along m or n (read into fragments with the transposing LDS load), every
+    output element against the oracle."""
+    M = N = K = 2048
+    a = S.tensor(M * K, "f16", seed=S.SEED_A)
+    b = S.tensor(K * N, "f16", seed=S.SEED_B)
+    kw = dict(a=lego.as_layout(getattr(lego, la_name)(M, K)), b=lego.as_layout(getattr(lego, lb_name)(K, N)))
+    plan = lego.gemm_plan(M, N, K, "f16", **kw)
+    say(f"gemm 2048 A {la_name} B {lb_name} plan={plan}")
+    assert "frtr" in plan
+    c = _run(lego, a, b, M, N, K, "f16", **kw).reshape(M, N)
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(getattr(OL, la_name)(M, K)),
+                OL.as_layout(getattr(OL, lb_name)(K, N)), "f16")
+    ok, mre, fre = OG.check_tolerance(c, r)
+    assert ok, (mre, fre)
