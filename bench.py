@@ -15,7 +15,9 @@ Also reported in the same JSON line:
                 average launch duration (fence-free HIP events between the
                 launches of the timed region, on the stream the kernels run on)
                 against the 8 TB/s HBM peak;
-  cpu_baseline  the CPU oracle timed on this host on a bounded sample.
+  cpu_baseline  the CPU oracle timed on this host on a bounded sample;
+  more          the other measured workloads (transposing and Morton remaps,
+                Morton-A GEMM, the four Row/Col operand layouts of the GEMM).
 """
 from __future__ import annotations
 
@@ -189,6 +191,134 @@ def bench_gemm(L, steps, warmup):
             "sha1": _source_sha1(L, "gemm", M=n, N=n, K=n, dtype="bf16")}
 
 
+def _alternate(L, la, lb, x, y, z, reps, warmup=5):
+    """Remaps la->lb (x -> y) and lb->la (y -> z), alternating, one event
+    between launches; mean ms of each direction.  z must equal x."""
+    import torch
+    for _ in range(warmup):
+        L.remap(la, lb, x, y)
+        L.remap(lb, la, y, z)
+    ev = HipEvents(2 * reps + 1, _stream())
+    torch.cuda.synchronize()
+    for k in range(reps):
+        ev.record(2 * k)
+        L.remap(la, lb, x, y)
+        ev.record(2 * k + 1)
+        L.remap(lb, la, y, z)
+    ev.record(2 * reps)
+    torch.cuda.synchronize()
+    f = sum(ev.ms(2 * k, 2 * k + 1) for k in range(reps)) / reps
+    i = sum(ev.ms(2 * k + 1, 2 * k + 2) for k in range(reps)) / reps
+    ev.close()
+    assert torch.equal(z, x), "remap round trip is not the identity"
+    return f, i
+
+
+def _flushed(L, la, lb, x, y, z, scratch, reps):
+    """Like _alternate, but a 1 GiB fill (not timed) evicts the 256 MB
+    last-level cache before every launch."""
+    import torch
+    ev = HipEvents(4 * reps, _stream())
+    torch.cuda.synchronize()
+    for k in range(reps):
+        scratch.fill_(k)
+        ev.record(4 * k)
+        L.remap(la, lb, x, y)
+        ev.record(4 * k + 1)
+        scratch.fill_(k + 0.5)
+        ev.record(4 * k + 2)
+        L.remap(lb, la, y, z)
+        ev.record(4 * k + 3)
+    torch.cuda.synchronize()
+    f = sum(ev.ms(4 * k, 4 * k + 1) for k in range(reps)) / reps
+    i = sum(ev.ms(4 * k + 2, 4 * k + 3) for k in range(reps)) / reps
+    ev.close()
+    assert torch.equal(z, x), "remap round trip is not the identity"
+    return f, i
+
+
+def _gemm_ms(L, a_buf, b_buf, c_buf, n, dtype, reps, **kw):
+    import torch
+    for _ in range(3):
+        L.gemm(a_buf, b_buf, c_buf, n, n, n, dtype, **kw)
+    ev = HipEvents(reps + 1, _stream())
+    torch.cuda.synchronize()
+    for k in range(reps):
+        ev.record(k)
+        L.gemm(a_buf, b_buf, c_buf, n, n, n, dtype, **kw)
+    ev.record(reps)
+    torch.cuda.synchronize()
+    ms = ev.ms(0, reps) / reps
+    ev.close()
+    return ms
+
+
+def bench_extra(L, reps=20):
+    """The other measured workloads: transposing remaps (Row <-> Col fp32,
+    the 2D transpose of Section V-C), Row <-> Morton fp16 4096^2 hot and with
+    the last-level cache flushed, the 4096^3 fp16 GEMM with A in Morton order
+    and B row-major, and the four Row/Col operand layouts of an 8192^3 fp16
+    GEMM (Section V-A)."""
+    import torch
+    import synth_inputs as S
+
+    def gbps(nbytes, ms):
+        return round(nbytes / (ms * 1e-3) / 1e9, 1)
+
+    out = {}
+    tr = []
+    for n in (2048, 4096, 8192):
+        x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()
+        y, z = torch.empty_like(x), torch.empty_like(x)
+        row, col = L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n))
+        f, i = _alternate(L, row, col, x, y, z, reps)
+        nb = 2 * n * n * 4
+        tr.append({"n": n, "bytes_per_launch": nb, "row_to_col_GBps": gbps(nb, f), "col_to_row_GBps": gbps(nb, i),
+                   "frac_hbm": round(2 * nb / ((f + i) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                   "plan": L.remap_plan(row, col, 4)["info"]})
+        del x, y, z
+    out["transpose_f32"] = tr
+
+    n = 4096
+    x = S.tensor(n * n, "f16", seed=S.SEED_SRC).cuda()
+    y, z = torch.empty_like(x), torch.empty_like(x)
+    row, mz = L.as_layout(L.Row(n, n)), L.as_layout(L.GenP("morton", [n, n]))
+    nb = 2 * n * n * 2
+    f, i = _alternate(L, row, mz, x, y, z, reps)
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    ff, fi = _flushed(L, row, mz, x, y, z, scratch, reps)
+    del scratch
+    out["morton_f16_4096"] = {"bytes_per_launch": nb, "hot_row_to_morton_GBps": gbps(nb, f),
+                              "hot_morton_to_row_GBps": gbps(nb, i), "flushed_row_to_morton_GBps": gbps(nb, ff),
+                              "flushed_morton_to_row_GBps": gbps(nb, fi),
+                              "plan": L.remap_plan(row, mz, 2)["info"]}
+
+    a_log = S.tensor(n * n, "f16", seed=S.SEED_A).cuda()
+    a_mz = torch.empty_like(a_log)
+    L.remap(row, mz, a_log, a_mz)
+    b = S.tensor(n * n, "f16", seed=S.SEED_B).cuda()
+    c = torch.empty(n * n, dtype=torch.float32, device="cuda")
+    kw = dict(a=mz, b=L.as_layout(L.Row(n, n)))
+    ms = _gemm_ms(L, a_mz, b, c, n, "f16", reps, **kw)
+    tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    out["gemm_morton_a_f16_4096"] = {"tflops": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
+                                     "plan": L.gemm_plan(n, n, n, "f16", **kw)}
+    del a_log, a_mz, b, c
+
+    n = 8192
+    a = S.tensor(n * n, "f16", seed=S.SEED_A).cuda()
+    b = S.tensor(n * n, "f16", seed=S.SEED_B).cuda()
+    c = torch.empty(n * n, dtype=torch.float32, device="cuda")
+    var = {}
+    for la in ("Row", "Col"):
+        for lb in ("Row", "Col"):
+            kw = dict(a=L.as_layout(getattr(L, la)(n, n)), b=L.as_layout(getattr(L, lb)(n, n)))
+            ms = _gemm_ms(L, a, b, c, n, "f16", 10, **kw)
+            var[f"A {la} B {lb}"] = round(2.0 * n ** 3 / (ms * 1e-3) / 1e12, 1)
+    out["gemm_operand_layouts_f16_8192_tflops"] = var
+    return out
+
+
 def cpu_baseline_remap(rounds=2):
     """The oracle remap of the full 8192^2 fp32 tensor, forward and back,
     ``rounds`` times, timed on this host."""
@@ -241,6 +371,8 @@ def main():
     ap.add_argument("--gemm-steps", type=int, default=20)
     ap.add_argument("--no-gemm", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip the other workloads (transposes, Morton, "
+                                                            "operand-layout GEMMs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the layout remap and GEMM kernels run on a single MI355X; "
@@ -300,6 +432,8 @@ def main():
         }
         if not args.no_cpu_baseline:
             out["gemm"]["cpu_baseline"] = cpu_baseline_gemm(g["a"], g["b"])
+    if not args.no_extra:
+        out["more"] = bench_extra(L)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_remap()
     print(json.dumps(out), flush=True)
