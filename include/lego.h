@@ -132,6 +132,10 @@ lego_status lego_expandby(int d, const int64_t* n, const int64_t* n_expanded, le
 lego_status lego_layout_rank(lego_layout_t l, int* rank);
 lego_status lego_layout_dims(lego_layout_t l, int cap, int64_t* dims);
 lego_status lego_layout_size(lego_layout_t l, int64_t* n); /* logical points */
+/* Physical positions: the original extents' product for an ExpandBy layout
+ * (Figure 9), the logical size otherwise.  A buffer in this layout holds this
+ * many elements. */
+lego_status lego_layout_phys_size(lego_layout_t l, int64_t* n);
 
 /* Host evaluation (Figures 4-5).  apply: idx[rank] logical -> *flat physical.
  * inv: physical flat -> idx[rank].  Errors: OUT_OF_RANGE. */
@@ -161,9 +165,14 @@ lego_status lego_inv_all_device(lego_layout_t l, int idx_bytes, void* d_out, voi
 
 /* Remap: for every logical x, the element at src.apply(x) of d_src moves to
  * dst.apply(x) of d_dst (elem_bytes = 1, 2, 4 or 8; the copy is bit-exact).
- * The layouts must have equal logical dims.  d_src and d_dst must not overlap
- * and must be 16-byte aligned.  Errors: INVALID_ARG, SIZE_MISMATCH,
- * UNSUPPORTED (ExpandBy), JIT, HIP. */
+ * The layouts must have equal logical dims.  d_src holds src's physical size
+ * in elements and d_dst dst's (they differ from the logical size only for
+ * ExpandBy layouts, Section III-D / Figure 9).  With an ExpandBy source, a
+ * destination position whose logical point lies outside the source's original
+ * extents (src.apply = -1) receives zero (padding); with an ExpandBy
+ * destination, logical points outside its extents are not copied (cropping).
+ * d_src and d_dst must not overlap and must be 16-byte aligned.  Errors:
+ * INVALID_ARG, SIZE_MISMATCH, UNSUPPORTED, JIT, HIP. */
 lego_status lego_remap(lego_layout_t src, lego_layout_t dst, int elem_bytes, const void* d_src, void* d_dst,
                        void* stream);
 

@@ -12,29 +12,45 @@ from __future__ import annotations
 
 import numpy as np
 
-from .layout import canon_unflatten, prod
+from .layout import ExpandBy, canon_unflatten, prod
 
 
-def remap(src_layout, dst_layout, src, chunk=1 << 22):
+def phys_size(layout):
+    """Number of physical positions of a layout: the original extents of an
+    ExpandBy (Figure 9), the logical size otherwise."""
+    return prod(layout.n) if isinstance(layout, ExpandBy) else prod(layout.dims())
+
+
+def remap(src_layout, dst_layout, src, chunk=1 << 22, fill=0):
     """Return dst with dst[L_dst.apply(x)] = src[L_src.apply(x)] for all x.
 
-    ``src`` is a flat numpy array of any dtype with prod(dims) elements.  The
-    logical index space is walked in chunks only to bound memory."""
+    ``src`` is a flat numpy array of any dtype with phys_size(L_src) elements;
+    dst has phys_size(L_dst) elements.  Under ExpandBy, apply gives -1 for a
+    point outside the original extents (Section III-D): such a point is not
+    written when it is the destination's, and writes ``fill`` when it is only
+    the source's (padding).  The logical index space is walked in chunks only
+    to bound memory."""
     dims = list(src_layout.dims())
     if list(dst_layout.dims()) != dims:
         raise ValueError("layouts have different logical shapes")
     n = prod(dims)
     src = np.asarray(src).reshape(-1)
-    if src.size != n:
+    if src.size != phys_size(src_layout):
         raise ValueError("source size does not match the layout")
-    dst = np.empty_like(src)
-    written = np.zeros(n, dtype=bool)
+    nd = phys_size(dst_layout)
+    dst = np.full(nd, fill, dtype=src.dtype)
+    written = np.zeros(nd, dtype=bool)
     for lo in range(0, n, chunk):
         x = np.arange(lo, min(n, lo + chunk), dtype=np.int64)
         coords = canon_unflatten(dims, x)
         s = np.asarray(src_layout.apply(coords), dtype=np.int64)
         d = np.asarray(dst_layout.apply(coords), dtype=np.int64)
-        dst[d] = src[s]
+        keep = d >= 0
+        s, d = s[keep], d[keep]
+        if written[d].any():
+            raise ValueError("destination position written twice")
+        has = s >= 0
+        dst[d[has]] = src[s[has]]
         written[d] = True
     if not written.all():
         raise ValueError("destination layout is not onto: some positions never written")

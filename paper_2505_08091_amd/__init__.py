@@ -66,6 +66,7 @@ _SIGS = {
     "lego_layout_rank": ([_vp, ctypes.POINTER(ctypes.c_int)], ctypes.c_int),
     "lego_layout_dims": ([_vp, ctypes.c_int, c_i64p], ctypes.c_int),
     "lego_layout_size": ([_vp, c_i64p], ctypes.c_int),
+    "lego_layout_phys_size": ([_vp, c_i64p], ctypes.c_int),
     "lego_apply": ([_vp, c_i64p, c_i64p], ctypes.c_int),
     "lego_inv": ([_vp, ctypes.c_int64, c_i64p], ctypes.c_int),
     "lego_verify_bijective": ([_vp, ctypes.c_int64], ctypes.c_int),
@@ -205,6 +206,12 @@ class Layout(_Handle):
         _check(_lib.lego_layout_size(self.h, ctypes.byref(n)))
         return n.value
 
+    def phys_size(self):
+        """Elements of a buffer in this layout (ExpandBy: the original extents)."""
+        n = ctypes.c_int64()
+        _check(_lib.lego_layout_phys_size(self.h, ctypes.byref(n)))
+        return n.value
+
     def apply(self, idx):
         if len(idx) != self.rank():
             raise LegoError(-1, "index rank differs from the layout rank")
@@ -286,8 +293,19 @@ def inv_all_device(layout, out, stream=None):
     _check(_lib.lego_inv_all_device(layout.h, out.element_size(), _ptr(out), _stream(stream)))
 
 
+def _need(t, n, what):
+    # the kernels index up to n elements of the buffer
+    if t.numel() < n:
+        raise LegoError(-2, f"{what} holds {t.numel()} elements, the layout needs {n}")
+
+
 def remap(src_layout, dst_layout, src, dst, stream=None):
-    """dst[dst.apply(x)] = src[src.apply(x)] for all logical x (cuda tensors)."""
+    """dst[dst.apply(x)] = src[src.apply(x)] for all logical x (cuda tensors);
+    positions of dst outside an ExpandBy source's extents become zero."""
+    if src.element_size() != dst.element_size():
+        raise LegoError(-1, "source and destination element sizes differ")
+    _need(src, src_layout.phys_size(), "source")
+    _need(dst, dst_layout.phys_size(), "destination")
     _check(_lib.lego_remap(src_layout.h, dst_layout.h, src.element_size(), _ptr(src), _ptr(dst), _stream(stream)))
 
 
@@ -314,6 +332,8 @@ def _desc(M, N, K, dtype, a=None, b=None, c=None, sched=None, lds_a=None, lds_b=
 
 def gemm(A, B, C, M, N, K, dtype, stream=None, **kw):
     """C (fp32) = A @ B with operands in their layouts (cuda tensors)."""
+    for t, lay, n, what in ((A, kw.get("a"), M * K, "A"), (B, kw.get("b"), K * N, "B"), (C, kw.get("c"), M * N, "C")):
+        _need(t, lay.phys_size() if lay is not None else n, what)
     d = _desc(M, N, K, dtype, **kw)
     _check(_lib.lego_gemm(ctypes.byref(d), _ptr(A), _ptr(B), _ptr(C), _stream(stream)))
 

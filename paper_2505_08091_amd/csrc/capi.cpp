@@ -272,6 +272,14 @@ lego_status lego_layout_size(lego_layout_t l, int64_t* n) {
   });
 }
 
+lego_status lego_layout_phys_size(lego_layout_t l, int64_t* n) {
+  return guard([&] {
+    if (!n) throw std::invalid_argument("null output");
+    *n = layout_of(l)->phys_size();
+    return LEGO_OK;
+  });
+}
+
 lego_status lego_apply(lego_layout_t l, const int64_t* idx, int64_t* flat) {
   return guard([&] {
     auto lay = layout_of(l);
@@ -381,8 +389,8 @@ lego_status lego_remap(lego_layout_t src, lego_layout_t dst, int elem_bytes, con
     if (!d_src || !d_dst) throw std::invalid_argument("null device pointer");
     if (((uintptr_t)d_src | (uintptr_t)d_dst) & 15) throw std::invalid_argument("buffers must be 16-byte aligned");
     if (s->dims() != d->dims()) throw std::length_error("remap layouts have different logical shapes");
-    i64 bytes = s->size() * elem_bytes;
-    if ((const char*)d_src < (char*)d_dst + bytes && (char*)d_dst < (const char*)d_src + bytes)
+    const i64 sbytes = s->phys_size() * elem_bytes, dbytes = d->phys_size() * elem_bytes;
+    if ((const char*)d_src < (char*)d_dst + dbytes && (char*)d_dst < (const char*)d_src + sbytes)
       throw std::invalid_argument("source and destination overlap");
     auto plan = remap_plan_cached(s, d, elem_bytes);
     void* a = const_cast<void*>(d_src);

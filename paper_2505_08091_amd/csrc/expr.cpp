@@ -199,10 +199,69 @@ Sum exact_div(const Ctx& c, const Sum& H, i64 n) {
   return canon(c, H.c0 / n, ts);
 }
 
+// x = A + B with A a multiple of g (its constant and every coefficient), B in
+// [0, g) and g a power of two dividing n; tries the largest such g first.
+// Then (A + B) div n = A div n, (A + B) mod n = (A mod n) + B and
+// A + B < n  <=>  A < n.  This is what keeps a vector of g consecutive
+// positions together under a modulus that is not a power of two.
+i64 gcd64(i64 a, i64 b) {
+  a = a < 0 ? -a : a;
+  b = b < 0 ? -b : b;
+  while (b) {
+    i64 t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+// A divisor every value of the atom is known to have.
+i64 atom_multiple(const Atom& a);
+
+}  // namespace
+
+i64 known_multiple(const Sum& s) {
+  i64 g = s.c0;
+  for (const Term& t : s.t) g = gcd64(g, t.c * atom_multiple(*t.a));
+  return g;
+}
+
+namespace {
+
+i64 atom_multiple(const Atom& a) {
+  switch (a.op) {
+    case Op::Mod: return gcd64(known_multiple(a.kids[0]), a.k);
+    case Op::Mul: return known_multiple(a.kids[0]) * known_multiple(a.kids[1]);
+    case Op::Select: return gcd64(known_multiple(a.kids[1]), known_multiple(a.kids[2]));
+    default: return 1;
+  }
+}
+
+bool split_aligned(const Sum& x, i64 n, Sum* A, Sum* B) {
+  if (n <= 1) return false;
+  for (i64 g = n & -n; g >= 2; g >>= 1) {
+    if (x.c0 % g) continue;
+    Sum a, b;
+    a.c0 = x.c0;
+    for (const Term& t : x.t) ((t.c * atom_multiple(*t.a)) % g == 0 ? a : b).t.push_back(t);
+    if (b.t.empty() || a.t.empty()) continue;
+    Interval rb = range(b);
+    if (rb.lo >= 0 && rb.hi < g) {
+      *A = a;
+      *B = b;
+      return true;
+    }
+  }
+  return false;
+}
+
 Sum div_atom(const Ctx& c, const Sum& L, i64 n) {
   if (L.is_const()) return cst(floordiv(L.c0, n));
   Interval r = range(L);
   if (r.lo >= 0 && r.hi < n) return cst(0);
+  {
+    Sum A, B;
+    if (split_aligned(L, n, &A, &B)) return fdiv(c, A, n);
+  }
   if (L.c0 == 0 && L.t.size() == 1 && L.t[0].c == 1) {
     const Atom& a = *L.t[0].a;
     if (a.op == Op::Div && range(a.kids[0]).lo >= 0) return div_atom(c, a.kids[0], a.k * n);
@@ -216,6 +275,10 @@ Sum mod_atom(const Ctx& c, const Sum& L, i64 n) {
   if (L.is_const()) return cst(floormod(L.c0, n));
   Interval r = range(L);
   if (r.lo >= 0 && r.hi < n) return L;
+  {
+    Sum A, B;
+    if (split_aligned(L, n, &A, &B)) return add(c, fmod(c, A, n), B);
+  }
   if (L.c0 == 0 && L.t.size() == 1 && L.t[0].c == 1) {
     const Atom& a = *L.t[0].a;
     if (a.op == Op::Field && (a.b == 0 || a.b % n == 0)) return atom_sum(make_field(c, a.var, a.a, n));
@@ -310,10 +373,14 @@ Sum bxor(const Ctx& c, const Sum& x, const Sum& y) {
 }
 
 Sum lt(const Ctx& c, const Sum& x, const Sum& y) {
-  (void)c;
   Interval rx = range(x), ry = range(y);
   if (rx.hi < ry.lo) return cst(1);
   if (rx.lo >= ry.hi) return cst(0);
+  // A vector of g consecutive positions shares one bounds test.
+  if (y.is_const() && y.c0 > 0) {
+    Sum A, B;
+    if (split_aligned(x, y.c0, &A, &B)) return lt(c, A, y);
+  }
   return atom_sum(make_op(Op::Lt, {x, y}, 0, {0, 1}));
 }
 

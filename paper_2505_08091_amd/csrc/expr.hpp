@@ -90,6 +90,10 @@ Sum isqrt(const Ctx& c, const Sum& x);
 Interval range(const Sum& s);
 std::string key(const Sum& s);
 bool depends_on(const Sum& s, int v);
+// A positive divisor of every value s can take (from its constant, its
+// coefficients and divisibility through mod, products and selects); 0 if s is
+// identically zero.
+i64 known_multiple(const Sum& s);
 void vars_of(const Sum& s, std::vector<bool>& used);
 
 // Replace variable v by an expression.

@@ -97,10 +97,7 @@ bool contiguous_in(const Sum& off, int e, int v) {
   if (ep.c0 != 0 || ep.t.size() != 1 || ep.t[0].c != 1) return false;
   const Atom& a = *ep.t[0].a;
   if (a.op != Op::Field || a.var != e || a.a != 1 || a.b != 0) return false;
-  if (rest.c0 % v) return false;
-  for (auto& t : rest.t)
-    if (t.c % v) return false;
-  return true;
+  return known_multiple(rest) % v == 0;
 }
 
 struct Operand {

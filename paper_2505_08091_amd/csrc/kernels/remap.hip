@@ -7,6 +7,8 @@
 //   LEGO_FN IDX_T src_vec(IDX_T t)   source vector index of destination vector t
 //   LEGO_FN IDX_T blk(IDX_T b)       destination chunk of schedule position b
 //   NBLK                             number of chunks
+//   MASKED, LEGO_FN IDX_T src_ok(IDX_T t)   1: vector t has a source (an
+//                                    ExpandBy source, Figure 9); else it is zero
 // LDS path (both sides are digit permutations; a tile of TILE elements is read
 // in source order into LDS and written in destination order):
 //   TILE, NT, VL, VS, LDSW_CONTIG
@@ -37,7 +39,11 @@ LEGO_FN void remap_chunk(const vec_t* __restrict__ src, vec_t* __restrict__ dst,
 #pragma unroll
   for (int u = 0; u < UNROLL; ++u) {
     const u64 t = base + (u64)u * NT;
+#if MASKED
+    if (t < NVEC) v[u] = src_ok((IDX_T)t) ? LEGO_LD(src + src_vec((IDX_T)t)) : (vec_t){};
+#else
     if (t < NVEC) v[u] = LEGO_LD(src + src_vec((IDX_T)t));
+#endif
   }
 #pragma unroll
   for (int u = 0; u < UNROLL; ++u) {

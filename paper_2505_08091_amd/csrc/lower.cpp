@@ -96,6 +96,22 @@ Sum remap_map(Ctx& c, const Layout& src, const Layout& dst, int p) {
   return src.apply(al, dst.inv(al, var(c, p)));
 }
 
+Sum remap_map_masked(Ctx& c, const Layout& src, const Layout& dst, int p, Sum* valid) {
+  SymAlg al{&c};
+  std::vector<Sum> x = dst.inv(al, var(c, p));
+  if (!src.expand_inner) {
+    *valid = cst(1);
+    return src.apply(al, x);
+  }
+  // ExpandBy apply (Figure 9) with its two outcomes kept apart: the point in
+  // the original extents, and whether it lies inside them.
+  std::vector<Sum> ip = unflatten(al, src.ne, src.expand_inner->apply(al, x));
+  Sum ok = cst(1);
+  for (size_t k = 0; k < src.en.size(); ++k) ok = al.mul(ok, al.lt(ip[k], al.c(src.en[k])));
+  *valid = ok;
+  return flatten(al, src.en, ip);
+}
+
 const char* prelude_text() {
   return R"PRELUDE(
 typedef unsigned int u32;

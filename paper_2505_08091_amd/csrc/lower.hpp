@@ -45,6 +45,10 @@ FnSpec spec_apply_flat(Ctx& c, const Layout& l);
 FnSpec spec_inv_flat(Ctx& c, const Layout& l);
 // src = L_src.apply(L_dst.inv(p)) for the destination physical index p.
 Sum remap_map(Ctx& c, const Layout& src, const Layout& dst, int p);
+// The same map for an ExpandBy source without its -1 branch: returns the source
+// position of destination position p assuming it is inside the original
+// extents, and sets *valid to the 0/1 test that it is (1 for other sources).
+Sum remap_map_masked(Ctx& c, const Layout& src, const Layout& dst, int p, Sum* valid);
 
 // The common prelude of every generated source: index types, LEGO_FN and the
 // helpers an expression may call (floor division of possibly negative values,

@@ -151,17 +151,22 @@ RemapPlan plan_remap(const Layout& src, const Layout& dst, int elem_bytes) {
 static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_bytes, bool allow_lds) {
   const char* et = elem_type(elem_bytes);
   if (src.dims() != dst.dims()) throw std::length_error("remap layouts have different logical shapes");
-  if (src.expand_inner || dst.expand_inner) throw Unsupported("remap of ExpandBy layouts is not supported");
-  const i64 N = src.size();
+  // Destination positions are enumerated (an ExpandBy destination has its
+  // original extents only); an ExpandBy source leaves some of them without a
+  // source element (Figure 9's -1): those receive zero.
+  const bool masked = (bool)src.expand_inner;
+  const i64 N = dst.phys_size();
+  const i64 NS = src.phys_size();
   const int maxv = std::max(1, 16 / elem_bytes);
   RemapPlan R;
 
   // M(p) = L_src.apply(L_dst.inv(p)) in the canonical digit form.
   Ctx c0;
   int p = c0.var("p", N);
-  Sum M = remap_map(c0, src, dst, p);
+  Sum VALID;
+  Sum M = remap_map_masked(c0, src, dst, p, &VALID);
   std::vector<Digit> digits;
-  bool pure = digits_of(c0, M, p, &digits);
+  bool pure = !masked && N == NS && digits_of(c0, M, p, &digits);
 
   i64 run = 1;
   if (pure) {
@@ -177,13 +182,15 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     Ctx c;
     int t = c.var("t", N / v), e = c.var("e", v);
     Sum pe = add(c, mulc(c, var(c, t), v), var(c, e));
-    Sum m = subst(c, remap_map(c, src, dst, c.var("p", N)), (int)c.vars.size() - 1, pe);
+    int pv = c.var("p", N);
+    Sum vv;
+    Sum m = subst(c, remap_map_masked(c, src, dst, pv, &vv), pv, pe);
+    // A vector is either wholly inside the source's extents or wholly outside.
+    if (depends_on(subst(c, vv, pv, pe), e)) continue;
     Sum ep, tp;
     if (!split_by(m, {e}, &ep, &tp)) continue;
     if (key(ep) != key(var(c, e))) continue;
-    bool ok = tp.c0 % v == 0;
-    for (auto& tt : tp.t) ok = ok && tt.c % v == 0;
-    if (ok) {
+    if (known_multiple(tp) % v == 0) {
       V = v;
       break;
     }
@@ -246,7 +253,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
       }
       std::sort(cd.begin(), cd.end(), [](const Dg& x, const Dg& y) { return x.c < y.c; });
     }
-    std::string fns = emit_all({{"blk",
+    std::vector<std::pair<std::string, std::function<FnSpec(Ctx&)>>> dfns = {{"blk",
                                  [&](Ctx& c) {
                                    int b = c.var("b", nblk);
                                    Sum o = var(c, b);
@@ -267,16 +274,29 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
                                  [&](Ctx& c) {
                                    int t = c.var("t", nvec);
                                    int pv = c.var("p", N);
-                                   Sum m = subst(c, remap_map(c, src, dst, pv), pv, mulc(c, var(c, t), V));
+                                   Sum vv;
+                                   Sum m = subst(c, remap_map_masked(c, src, dst, pv, &vv), pv, mulc(c, var(c, t), V));
                                    FnSpec f;
                                    f.params = {t};
                                    f.outs = {fdiv(c, m, V)};
                                    return f;
-                                 }}},
-                               &wide, &info);
+                                 }}};
+    if (masked)
+      dfns.push_back({"src_ok", [&](Ctx& c) {
+                        int t = c.var("t", nvec);
+                        int pv = c.var("p", N);
+                        Sum vv;
+                        remap_map_masked(c, src, dst, pv, &vv);
+                        FnSpec f;
+                        f.params = {t};
+                        f.outs = {subst(c, vv, pv, mulc(c, var(c, t), V))};
+                        return f;
+                      }});
+    std::string fns = emit_all(dfns, &wide, &info);
     s << header() << "#define ELEM_T " << et << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define V " << V
       << "\n#define NVEC " << nvec << "ull\n#define NBLK " << nblk << "ull\n#define NT " << NT << "\n#define UNROLL " << UNROLL
-      << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_DIRECT 1\n"
+      << "\n#define NONTEMPORAL " << nontemporal << "\n#define MASKED " << (masked ? 1 : 0) << "\n#define NSRC " << NS
+      << "ull\n#define LEGO_REMAP_DIRECT 1\n"
       << fns << "// ---- template ----\n" << tpl_remap;
     R.kernel = "lego_remap_direct";
     R.block = NT;
@@ -289,7 +309,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     R.src = s.str();
     R.info = std::string(R.path == REMAP_DIRECT ? "direct" : "gather") + (src_order ? " src-order" : " dst-order") +
              " NT=" + std::to_string(NT) + " UNROLL=" + std::to_string(UNROLL) + " V=" + std::to_string(V) +
-             " run=" + std::to_string(run) + info;
+             " run=" + std::to_string(run) + (masked ? " masked" : "") + info;
     return R;
   }
 
@@ -385,8 +405,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     Sum kd = kd_from_ks(c, add(c, mulc(c, var(c, q), VL), var(c, e)));
     Sum ep, qp;
     if (split_by(kd, {e}, &ep, &qp) && key(ep) == key(var(c, e))) {
-      contig = qp.c0 % VL == 0;
-      for (auto& t : qp.t) contig = contig && t.c % VL == 0;
+      contig = known_multiple(qp) % VL == 0;
     }
   }
   // A VL-run longer than a swizzled VS-vector may be split by the swizzle.

@@ -52,8 +52,8 @@ def test_version_and_last_error(lego):
     (lambda L: L.gemm_plan(256, 256, 256, "f16", a=L.as_layout(L.Row(128, 256))), "SIZE_MISMATCH"),
     (lambda L: L.remap_plan(L.as_layout(L.Row(4, 4)), L.as_layout(L.Row(2, 8)), 4), "SIZE_MISMATCH"),
     (lambda L: L.remap_plan(L.as_layout(L.Row(4, 4)), L.as_layout(L.Row(4, 4)), 3), "INVALID_ARG"),
-    (lambda L: L.remap_plan(L.ExpandBy([3, 3], [4, 4], L.as_layout(L.Row(4, 4))),
-                            L.ExpandBy([3, 3], [4, 4], L.as_layout(L.Row(4, 4))), 4), "UNSUPPORTED"),
+    (lambda L: L.gemm_plan(64, 64, 64, "f16", a=L.ExpandBy([60, 64], [64, 64], L.as_layout(L.Row(64, 64)))),
+     "UNSUPPORTED"),
     (lambda L: L.mfma_fragment_layout(7, 0), "INVALID_ARG"),
 ])
 def test_error_codes(lego, call, status):
@@ -154,3 +154,25 @@ def test_plans_choose_expected_paths(lego):
     assert p["path"] == "gather"
     info = L.gemm_plan(8192, 8192, 8192, "bf16")
     assert "direct-lds" in info and "A:V8k sep" in info and "frvec" in info
+
+
+def test_binding_checks_buffer_sizes_before_launch(lego):
+    """The binding refuses buffers smaller than a layout's physical size
+    (checked on the host, before any device call)."""
+    import torch
+    r = lego.as_layout(lego.Row(8, 8))
+    e = lego.ExpandBy([5, 7], [8, 8], lego.as_layout(lego.Row(8, 8)))
+    assert e.size() == 64 and e.phys_size() == 35 and r.phys_size() == 64
+    with pytest.raises(lego.LegoError) as err:
+        lego.remap(r, r, torch.zeros(63), torch.zeros(64))
+    assert err.value.status == "SIZE_MISMATCH"
+    with pytest.raises(lego.LegoError) as err:
+        lego.remap(e, r, torch.zeros(35), torch.zeros(40))
+    assert err.value.status == "SIZE_MISMATCH"
+    with pytest.raises(lego.LegoError) as err:
+        lego.remap(e, r, torch.zeros(35, dtype=torch.float16), torch.zeros(64))
+    assert err.value.status == "INVALID_ARG"
+    with pytest.raises(lego.LegoError) as err:
+        lego.gemm(torch.zeros(64 * 64, dtype=torch.float16), torch.zeros(64 * 63, dtype=torch.float16),
+                  torch.zeros(64 * 64), 64, 64, 64, "f16")
+    assert err.value.status == "SIZE_MISMATCH"

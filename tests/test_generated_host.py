@@ -57,15 +57,22 @@ int main(int argc, char** argv) {
       if (c >= nblk || hit[c]++) FAIL("blk is not a bijection");
     }
   }
-  std::vector<long long> perm(n, -1);  // dst element -> src element
+  const u64 nsrc = NSRC;
+  std::vector<long long> perm(n, -2);  // dst element -> src element (-1: zero fill)
   for (u64 t = 0; t < NVEC; ++t) {
+#if MASKED
+    if (!src_ok((IDX_T)t)) {
+      for (int e = 0; e < V; ++e) perm[t * V + e] = -1;
+      continue;
+    }
+#endif
     u64 s = (u64)src_vec((IDX_T)t);
-    if (s >= NVEC) FAIL("src_vec(%llu) = %llu out of range", (unsigned long long)t, (unsigned long long)s);
+    if ((s + 1) * V > nsrc) FAIL("src_vec(%llu) = %llu out of range", (unsigned long long)t, (unsigned long long)s);
     for (int e = 0; e < V; ++e) perm[t * V + e] = (long long)(s * V + e);
   }
 #else
-  const u64 n = NELEM;
-  std::vector<long long> perm(n, -1);
+  const u64 n = NELEM, nsrc = NELEM;
+  std::vector<long long> perm(n, -2);
   std::vector<long long> tile(TILE);
   std::vector<char> wseen(TILE);
   for (u64 g = 0; g < NTILES; ++g) {
@@ -86,17 +93,17 @@ int main(int argc, char** argv) {
       if (l % VS || l + VS > TILE) FAIL("ldsr out of range");
       if (d % VS || d + VS > n) FAIL("dst_off out of range");
       for (int e = 0; e < VS; ++e) {
-        if (perm[d + e] != -1) FAIL("destination written twice");
+        if (perm[d + e] != -2) FAIL("destination written twice");
         if (tile[l + e] < 0) FAIL("LDS slot read before written");
         perm[d + e] = tile[l + e];
       }
     }
   }
 #endif
-  std::vector<char> seen(n);
+  std::vector<char> seen(nsrc);
   for (u64 i = 0; i < n; ++i) {
-    if (perm[i] < 0) FAIL("destination %llu never written", (unsigned long long)i);
-    if (seen[perm[i]]++) FAIL("source read twice");
+    if (perm[i] == -2) FAIL("destination %llu never written", (unsigned long long)i);
+    if (perm[i] >= 0 && seen[perm[i]]++) FAIL("source read twice");
   }
   FILE* f = fopen(argv[1], "wb");
   fwrite(perm.data(), 8, n, f);
@@ -324,8 +331,8 @@ def test_index_sources_of_gpu_cases():
 
 def _remap_cases():
     import paper_2505_08091_amd as L
-    from tests.test_gpu_remap import _small_cases
-    cases = [(n, ls, ld, ols, old) for n, ls, ld, ols, old in _small_cases(L)]
+    from tests.test_gpu_remap import _expand_cases, _small_cases
+    cases = [(n, ls, ld, ols, old) for n, ls, ld, ols, old in _small_cases(L) + _expand_cases(L)]
     for n in (2048, 4096, 1024):
         cases.append((f"transpose {n}", L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n)),
                       OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.Col(n, n))))
@@ -340,13 +347,14 @@ def test_remap_sources_of_gpu_cases(elem_bytes):
     with tempfile.TemporaryDirectory() as tmp:
         out = os.path.join(tmp, "out.bin")
         for name, ls, ld, ols, old in _remap_cases():
-            if ols.size() > (1 << 23) and elem_bytes != 4:
+            if OL.prod(ols.dims()) > (1 << 23) and elem_bytes != 4:
                 continue
             for a, b, oa, ob in ((ls, ld, ols, old), (ld, ls, old, ols)):
                 src = L.plan_source("remap", a, b, param=elem_bytes)
                 _compile_and_run(src, HARNESS_REMAP, tmp, [out])
                 perm = np.fromfile(out, dtype=np.int64)
-                exp = OR.remap(oa, ob, np.arange(oa.size(), dtype=np.int64))
+                # source element k is tagged k + 1, so zero fill reads as -1
+                exp = OR.remap(oa, ob, np.arange(1, OR.phys_size(oa) + 1, dtype=np.int64)) - 1
                 assert (perm == exp).all(), (name, elem_bytes)
 
 

@@ -87,6 +87,50 @@ def _small_cases(L):
     ]
 
 
+def _expand_cases(L):
+    """ExpandBy (Section III-D, Figure 9): compact arrays whose extents the
+    tiles do not divide, against tiled layouts of the padded shape."""
+    def pad(n, ne, inner_l, inner_o):
+        return L.ExpandBy(n, ne, inner_l), OL.ExpandBy(n, ne, inner_o)
+    out = []
+    for n, ne, tl, to in (
+            ([5, 7], [6, 8], L.TileOrderBy(L.Row(3, 2), L.Row(2, 4)), OL.TileOrderBy(OL.Row(3, 2), OL.Row(2, 4))),
+            ([1000, 1000], [1024, 1024], L.TileOrderBy(L.Col(16, 16), L.Row(64, 64)),
+             OL.TileOrderBy(OL.Col(16, 16), OL.Row(64, 64))),
+            ([999, 1001], [1024, 1024], L.TileOrderBy(L.Col(16, 16), L.Row(64, 64)),
+             OL.TileOrderBy(OL.Col(16, 16), OL.Row(64, 64)))):
+        ls, os_ = pad(n, ne, L.as_layout(L.Row(*ne)), OL.as_layout(OL.Row(*ne)))
+        out.append((f"pad {n[0]}x{n[1]} into tiles of {ne[0]}x{ne[1]}", ls, tl, os_, to))
+    return out
+
+
+@pytest.mark.parametrize("elem", ["f32", "f16", "i64", "u8"])
+def test_remap_expandby_pad_and_crop(lego, elem):
+    """Compact -> padded tiled buffer (zero padding) -> compact again."""
+    import torch
+    dev = need_gpu()
+    for name, ls, ld, ols, old in _expand_cases(lego):
+        ns, nd = OR.phys_size(ols), OR.phys_size(old)
+        if elem == "i64":
+            src = S.int_tensor(ns, bits=64)
+        elif elem == "u8":
+            src = (S.int_tensor(ns) % 251).to(torch.uint8)
+        else:
+            src = S.tensor(ns, elem, seed=7)
+        say(f"remap {name} {elem} plan={lego.remap_plan(ls, ld, src.element_size())['info']}")
+        d_src = src.to(dev)
+        d_pad = torch.full((nd,), 1, dtype=src.dtype, device=dev)  # padding must come back zero
+        lego.remap(ls, ld, d_src, d_pad)
+        torch.cuda.synchronize()
+        exp = OR.remap(ols, old, bits(src))
+        assert (bits(d_pad.cpu()) == exp).all(), name
+        say(f"remap crop {name} {elem} plan={lego.remap_plan(ld, ls, src.element_size())['info']}")
+        d_back = torch.empty_like(d_src)
+        lego.remap(ld, ls, d_pad, d_back)
+        torch.cuda.synchronize()
+        assert (bits(d_back.cpu()) == bits(src)).all(), name
+
+
 @pytest.mark.parametrize("elem", ["f32", "f16", "i64", "u8"])
 def test_remap_small_and_ragged(lego, elem):
     import torch

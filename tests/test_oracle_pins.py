@@ -368,6 +368,23 @@ def test_remap_transpose_matches_numpy():
     assert (out == src.reshape(n, m).T.ravel()).all()
 
 
+def test_remap_expandby_pads_and_crops_like_numpy():
+    """ExpandBy source (Figure 9): the compact 5x7 array lands in a 6x8 tiled
+    buffer with zero padding, equal to numpy's pad followed by the tile-major
+    reshape; the ExpandBy destination crops it back."""
+    data = np.arange(1, 36, dtype=np.int32)
+    src = L.ExpandBy([5, 7], [6, 8], L.as_layout(L.Row(6, 8)))
+    tiled = L.TileOrderBy(L.Row(3, 2), L.Row(2, 4))  # 2x4 tiles over [6, 8]
+    out = R.remap(src, tiled, data)
+    padded = np.pad(data.reshape(5, 7), ((0, 1), (0, 1)))
+    assert (out == padded.reshape(3, 2, 2, 4).transpose(0, 2, 1, 3).ravel()).all()
+    back = R.remap(tiled, src, out)
+    assert (back == data).all()
+    # row-major padding alone is numpy's pad, and a fill value is honoured
+    out2 = R.remap(src, L.as_layout(L.Row(6, 8)), data, fill=-7)
+    assert (out2 == np.pad(data.reshape(5, 7), ((0, 1), (0, 1)), constant_values=-7).ravel()).all()
+
+
 def test_remap_blocked_matches_numpy_reshape():
     """Row -> 2-level blocked (column-major tile order, row-major tiles) equals
     a numpy reshape/transpose of the same data."""
