@@ -110,6 +110,8 @@ struct Operand {
   i64 NVEC = 0;
   bool guard = false, sep = false, svec = false, frvec = false;
   bool frtr = false;      // fragments read with the transposing LDS load
+  i64 rows_total = 0;     // M (A) or N (B): logical extent along the tile rows
+  bool edge = false;      // some loads fall outside the operand (padded tiles)
   bool user_lds = false;  // LDS layout given by the caller
   bool direct = false;  // load vector q fills LDS slot q (direct global-to-LDS copy)
 };
@@ -120,9 +122,17 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   GemmRequest rq = rq0;
   if (rq.dtype != LEGO_F16 && rq.dtype != LEGO_BF16) throw std::invalid_argument("GEMM inputs must be fp16 or bf16");
   if (rq.M <= 0 || rq.N <= 0 || rq.K <= 0) throw std::invalid_argument("GEMM sizes must be positive");
-  if (!rq.bm) rq.bm = (int)std::min<i64>(256, rq.M);
-  if (!rq.bn) rq.bn = (int)std::min<i64>(256, rq.N);
-  if (!rq.bk) rq.bk = (int)std::min<i64>(64, rq.K);
+  // Default tiles: 64, 128 or 256 rows (the smallest covering the extent, at
+  // most 256), 64-deep k-steps (32 for K < 64); extents they do not divide get
+  // padded tiles.
+  auto pick = [](i64 n) {
+    i64 t = 64;
+    while (t < 256 && t < n) t *= 2;
+    return (int)t;
+  };
+  if (!rq.bm) rq.bm = pick(rq.M);
+  if (!rq.bn) rq.bn = pick(rq.N);
+  if (!rq.bk) rq.bk = rq.K >= 64 ? 64 : 32;
   // Default wave tiles keep at most 8 MFMA blocks (128 fp32 accumulators) per
   // wave, so accumulators stay in VGPRs and two waves share each SIMD.
   if (!rq.wm) rq.wm = rq.bm >= 256 ? 128 : (rq.bm >= 64 ? rq.bm / 2 : rq.bm);
@@ -131,7 +141,10 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   const i64 M = rq.M, N = rq.N, K = rq.K;
   const int bm = rq.bm, bn = rq.bn, bk = rq.bk, wm = rq.wm, wn = rq.wn;
   if (bm <= 0 || bn <= 0 || bk <= 0 || wm <= 0 || wn <= 0) throw std::invalid_argument("tile sizes must be positive");
-  if (M % bm || N % bn || K % bk) throw Unsupported("GEMM sizes must be multiples of the workgroup tile");
+  // Sizes the tiles do not divide are padded to whole tiles (the partial tiles
+  // of Section III-D): loads outside [M, K] / [K, N] read zero, stores outside
+  // [M, N] are dropped.
+  const bool edge_m = M % bm != 0, edge_n = N % bn != 0, edge_k = K % bk != 0;
   const int MB = (wm % 32 == 0 && wn % 32 == 0) ? 32 : 16;
   const int KB = MB == 32 ? 16 : 32;
   if (wm % MB || wn % MB || bm % wm || bn % wn || bk % KB)
@@ -142,7 +155,7 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   if (MI * NI * NREG > 256) throw Unsupported("wave tile needs more than 256 accumulator registers");
   const i64 lds_bytes = 2ll * (bm + bn) * bk * 2;
   if (lds_bytes > 160 * 1024) throw Unsupported("two LDS stages exceed 160 KiB");
-  const i64 Mt = M / bm, Nt = N / bn, Kt = K / bk, P = Mt * Nt;
+  const i64 Mt = (M + bm - 1) / bm, Nt = (N + bn - 1) / bn, Kt = (K + bk - 1) / bk, P = Mt * Nt;
 
   LayoutP LA = rq.a ? rq.a : make_from_piece(make_row({M, K}));
   LayoutP LB = rq.b ? rq.b : make_from_piece(make_col({K, N}));
@@ -152,13 +165,19 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   need_dims(LC, {M, N}, "C");
   const i64 G = std::min<i64>(rq.group_m, Mt);
   LayoutP SCH = rq.sched;
+  // Grouped order with a ragged last group (Mt % G rows): the full groups are
+  // the layout RegP([Mt/G, G, Nt], [1, 3, 2]); the last Mt % G tile rows form one
+  // more group in the same column-major order.
+  const bool ragged_groups = !SCH && G > 1 && Mt % G != 0;
   if (!SCH) {
     if (Mt % G == 0 && G > 1)
       SCH = make_orderby(make_groupby({Mt, Nt}), {make_regp({Mt / G, G, Nt}, {1, 3, 2})});
+    else if (ragged_groups && Mt / G > 0)
+      SCH = make_orderby(make_groupby({Mt / G * G, Nt}), {make_regp({Mt / G, G, Nt}, {1, 3, 2})});
     else
       SCH = make_from_piece(make_row({Mt, Nt}));
   }
-  need_dims(SCH, {Mt, Nt}, "schedule");
+  if (!ragged_groups) need_dims(SCH, {Mt, Nt}, "schedule");
   const bool xcd = rq.xcd && P % 8 == 0;
   LayoutP XCD = xcd ? make_orderby(make_groupby({P / 8, 8}), {make_regp({P / 8, 8}, {2, 1})}) : nullptr;
   LayoutP SA = rq.lds_a ? rq.lds_a : default_lds(bm, bk);
@@ -171,6 +190,17 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   Operand ops[2] = {{bm, bk, LA, SA, false}, {bn, bk, LB, SB, true}};
   ops[0].user_lds = (bool)rq.lds_a;
   ops[1].user_lds = (bool)rq.lds_b;
+  ops[0].rows_total = M;
+  ops[1].rows_total = N;
+  ops[0].edge = edge_m || edge_k;
+  ops[1].edge = edge_n || edge_k;
+  // Validity of tile element (i, j) at tile coordinates (tt, kt): inside the
+  // operand's logical extents.
+  auto in_range = [&](Ctx& c, const Operand& o, const Sum& tt, const Sum& kt, const Sum& i, const Sum& j) {
+    Sum row = add(c, mulc(c, tt, o.R), i);
+    Sum kk = add(c, mulc(c, kt, o.KD), j);
+    return mul(c, lt(c, row, cst(o.rows_total)), lt(c, kk, cst(K)));
+  };
   // With a single round of load vectors, only threads below NVEC load; giving
   // tid that range lets the range analysis prove separability.
   auto tid_ext = [&](const Operand& o) -> i64 { return o.NV == 1 ? std::min<i64>(NT, o.NVEC) : NT; };
@@ -220,7 +250,10 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
         Sum xs = add(c, mulc(c, var(c, x), v), var(c, e));
         Sum off = axis == 1 ? glob_off(c, o, var(c, tt), var(c, kt), var(c, y), xs)
                             : glob_off(c, o, var(c, tt), var(c, kt), xs, var(c, y));
-        if (contiguous_in(off, e, v)) {
+        // With padded tiles a vector must lie wholly inside or wholly outside.
+        Sum ok = axis == 1 ? in_range(c, o, var(c, tt), var(c, kt), var(c, y), xs)
+                           : in_range(c, o, var(c, tt), var(c, kt), xs, var(c, y));
+        if (contiguous_in(off, e, v) && !(o.edge && depends_on(ok, e))) {
           o.V = v;
           o.axis = axis;
           found = true;
@@ -316,6 +349,11 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
     Sum i, j;
     load_elem(c, t, var(c, tid), var(c, u), var(c, e), &i, &j);
     if (!contiguous_in(glob_off(c, t, var(c, tt), var(c, kt), i, j), e, 8)) direct = false;
+    // Padded tiles: whole-vector validity, and 32-bit byte offsets for the
+    // range-checked buffer loads that fill out-of-range slots with zero.
+    if (o.edge && (depends_on(in_range(c, t, var(c, tt), var(c, kt), i, j), e) ||
+                   2 * o.glob->phys_size() >= (i64(1) << 31)))
+      direct = false;
   }
   if (direct) {
     for (Operand& o : ops) {
@@ -359,7 +397,23 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
                    if (xcd) q = XCD->apply(al, unflatten(al, {P / 8, 8}, q));
                    FnSpec f;
                    f.params = {pid};
-                   f.outs = SCH->inv(al, q);
+                   if (!ragged_groups) {
+                     f.outs = SCH->inv(al, q);
+                     return f;
+                   }
+                   // Full groups first, then the ragged group of r = Mt % G rows.
+                   const i64 full = Mt / G * G, r = Mt % G, nfull = full * Nt;
+                   Sum rest = sub(c, q, cst(nfull));
+                   Sum tm_r = add(c, cst(full), fmod(c, rest, r)), tn_r = fdiv(c, rest, r);
+                   if (full == 0) {
+                     f.outs = {tm_r, tn_r};
+                     return f;
+                   }
+                   Sum in_full = lt(c, q, cst(nfull));
+                   // Clamp the argument of the full-group layout into its domain.
+                   Sum qf = select(c, in_full, q, cst(0));
+                   std::vector<Sum> g = SCH->inv(al, qf);
+                   f.outs = {select(c, in_full, g[0], tm_r), select(c, in_full, g[1], tn_r)};
                    return f;
                  }});
   const char* pre[2] = {"a_", "b_"};
@@ -440,6 +494,20 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
                      f.outs = {oo.lds->apply(al, {row, kk})};
                      return f;
                    }});
+    if (o.edge)
+      fns.push_back({p + "ok", [&, k](Ctx& c) {
+                       // 1 when load vector u of thread tid at tile (tt, kt) lies
+                       // inside the operand, 0 when it is padding.
+                       const Operand& oo = ops[k];
+                       int tt = c.var(oo.is_b ? "tn" : "tm", oo.is_b ? Nt : Mt), kt = c.var("kt", Kt),
+                           tid = c.var("tid", tid_ext(oo)), u = c.var("u", oo.NV);
+                       Sum i, j;
+                       load_elem(c, oo, var(c, tid), var(c, u), cst(0), &i, &j);
+                       FnSpec f;
+                       f.params = {tt, kt, tid, u};
+                       f.outs = {in_range(c, oo, var(c, tt), var(c, kt), i, j)};
+                       return f;
+                     }});
     if (o.frtr)
       fns.push_back({p + "ft", [&, k](Ctx& c) {
                        // Address lane `lane` supplies to the transposing read of
@@ -479,6 +547,23 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
                 add(c, mulc(c, var(c, *ni), MB), col));
     return LC->apply(al, {m, n});
   };
+  const bool cedge = edge_m || edge_n;
+  if (cedge)
+    fns.push_back({"c_ok", [&](Ctx& c) {
+                     int tm = c.var("tm", Mt), tn = c.var("tn", Nt), lane = c.var("lane", 64),
+                         w = c.var("w", NWAVES), mi = c.var("mi", MI), ni = c.var("ni", NI), r = c.var("r", NREG);
+                     SymAlg al{&c};
+                     Sum f0 = FC->apply(al, {var(c, lane), var(c, r)});
+                     Sum row = fdiv(c, f0, MB), col = fmod(c, f0, MB);
+                     Sum m = add(c, add(c, mulc(c, var(c, tm), bm), mulc(c, fdiv(c, var(c, w), NWN), wm)),
+                                 add(c, mulc(c, var(c, mi), MB), row));
+                     Sum n = add(c, add(c, mulc(c, var(c, tn), bn), mulc(c, fmod(c, var(c, w), NWN), wn)),
+                                 add(c, mulc(c, var(c, ni), MB), col));
+                     FnSpec f;
+                     f.params = {tm, tn, lane, w, mi, ni, r};
+                     f.outs = {mul(c, lt(c, m, cst(M)), lt(c, n, cst(N)))};
+                     return f;
+                   }});
   bool csep = false;
   {
     Ctx c;
@@ -540,8 +625,10 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       << "SEP " << (o.sep ? 1 : 0) << "\n#define " << P2[k] << "SVEC " << (o.svec ? 1 : 0) << "\n#define " << P2[k]
       << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "FRTR " << (o.frtr ? 1 : 0) << "\n#define " << P2[k]
       << "NVEC " << o.NVEC << "u\n#define " << P2[k]
-      << "GUARD " << (o.guard ? 1 : 0) << "\n";
+      << "GUARD " << (o.guard ? 1 : 0) << "\n#define " << P2[k] << "EDGE " << (o.edge ? 1 : 0) << "\n#define "
+      << P2[k] << "BYTES " << 2 * o.glob->phys_size() << "u\n";
   }
+  s << "#define C_EDGE " << (cedge ? 1 : 0) << "\n";
   // Two staging register sets when the accumulators live in AGPRs (one wave
   // per SIMD leaves the VGPRs for them); one otherwise, so two waves fit.
   int prefetch = (MI * NI * NREG > 128) ? 2 : 1;
@@ -568,7 +655,8 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
        << (ops[0].frvec ? " frvec" : (ops[0].frtr ? " frtr" : " frscalar")) << " B:V" << ops[1].V
        << (ops[1].gaxis ? "k" : "n") << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
        << (ops[1].frvec ? " frvec" : (ops[1].frtr ? " frtr" : " frscalar")) << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
-       << (direct ? " direct-lds" : " staged") << " stages " << nstages << " lds " << nstages * stage_bytes
+       << (direct ? " direct-lds" : " staged") << (ragged_groups ? " ragged-groups" : "")
+       << (ops[0].edge || ops[1].edge || cedge ? " edges" : "") << " stages " << nstages << " lds " << nstages * stage_bytes
        << "B ops" << opsinfo.str();
   g.info = info.str();
   return g;

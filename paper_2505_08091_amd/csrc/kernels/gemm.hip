@@ -28,6 +28,10 @@
 //                                    load: the address lane supplies for half h
 //   (b_* likewise with tn)
 //   c_t(tm, tn) c_l(lane, w, mi, ni, r)   or   c_f(tm, tn, lane, w, mi, ni, r)
+//   A_EDGE, a_ok(tm, kt, tid, u), A_BYTES (and B_*): tiles padded past the
+//       operand (Section III-D partial tiles): load vector u is inside (1) or
+//       padding (0, read as zero); the operand's size in bytes
+//   C_EDGE, c_ok(tm, tn, lane, w, mi, ni, r): the C element exists
 
 typedef unsigned short elem_t;
 typedef elem_t av_t __attribute__((ext_vector_type(A_V)));
@@ -141,6 +145,12 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
       if (A_GUARD && (IDX_T)u * NT + tid >= A_NVEC) continue;
+#if A_EDGE
+      if (!a_ok(tm, kt, tid, u)) {
+        ra[rbuf][u] = (av_t){};
+        continue;
+      }
+#endif
 #if A_SEP
       ra[rbuf][u] = *(const av_t*)(Ab + a_gk(kt) + a_loc[u]);
 #else
@@ -150,6 +160,12 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
       if (B_GUARD && (IDX_T)u * NT + tid >= B_NVEC) continue;
+#if B_EDGE
+      if (!b_ok(tn, kt, tid, u)) {
+        rb[rbuf][u] = (bv_t){};
+        continue;
+      }
+#endif
 #if B_SEP
       rb[rbuf][u] = *(const bv_t*)(Bb + b_gk(kt) + b_loc[u]);
 #else
@@ -258,6 +274,12 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // NSTAGES LDS stages form a ring: the tile for step kt+NSTAGES-1 is
   // requested at the top of step kt into the stage read during step kt-1.
   const IDX_T wu = __builtin_amdgcn_readfirstlane(tid / 64u);
+#if A_EDGE || B_EDGE
+  // Range-checked buffer loads: an offset past the buffer's end (0xFFFFFFFF
+  // for padding) writes zero to the LDS slot instead of reading memory.
+  const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)A_BYTES, 0x00020000);
+  const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)B, (short)0, (int)B_BYTES, 0x00020000);
+#endif
   auto dload = [&](IDX_T kt, int stage) {
     elem_t* la = lds + stage * STAGE;
     elem_t* lb = la + A_STAGE;
@@ -268,9 +290,13 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #else
       const elem_t* src = A + a_gf(tm, kt, tid, u);
 #endif
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                       (__attribute__((address_space(3))) void*)(la + ((IDX_T)u * NT + wu * 64u) * 8u),
-                                       16, 0, 0);
+      __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(la + ((IDX_T)u * NT + wu * 64u) * 8u);
+#if A_EDGE
+      const unsigned off = a_ok(tm, kt, tid, u) ? (unsigned)((src - A) * 2) : 0xFFFFFFFFu;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, dst, 16, off, 0, 0, 0);
+#else
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src, dst, 16, 0, 0);
+#endif
     }
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
@@ -279,9 +305,13 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #else
       const elem_t* src = B + b_gf(tn, kt, tid, u);
 #endif
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                       (__attribute__((address_space(3))) void*)(lb + ((IDX_T)u * NT + wu * 64u) * 8u),
-                                       16, 0, 0);
+      __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(lb + ((IDX_T)u * NT + wu * 64u) * 8u);
+#if B_EDGE
+      const unsigned off = b_ok(tn, kt, tid, u) ? (unsigned)((src - B) * 2) : 0xFFFFFFFFu;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, off, 0, 0, 0);
+#else
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src, dst, 16, 0, 0);
+#endif
     }
   };
   // s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt at their maxima).
@@ -403,6 +433,9 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     for (int j = 0; j < NI; ++j)
 #pragma unroll
       for (int r = 0; r < NREG; ++r) {
+#if C_EDGE
+        if (!c_ok(tm, tn, lane, w, i, j, r)) continue;
+#endif
 #if C_SEP
         __builtin_nontemporal_store(acc[i][j][r], Cb + c_l(lane, w, i, j, r));
 #else

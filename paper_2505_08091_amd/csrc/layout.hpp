@@ -190,8 +190,19 @@ struct Layout {
       for (size_t k = 0; k < en.size(); ++k) inside = al.mul(inside, al.lt(ip[k], al.c(en[k])));
       return al.sel(inside, flatten(al, en, ip), al.c(-1));
     }
-    typename A::V flat = flatten(al, g, i);
-    for (auto& o : chain) flat = o.apply(al, unflatten(al, o.dims(), flat));
+    // When the first OrderBy has exactly the logical dims, unflatten(flatten(i))
+    // is i itself: the piece then takes the coordinates directly, which keeps
+    // the lowered expression linear in them (and meaningful past the extents,
+    // as padded tiles need).
+    size_t k0 = 0;
+    typename A::V flat;
+    if (!chain.empty() && chain[0].dims() == g) {
+      flat = chain[0].apply(al, i);
+      k0 = 1;
+    } else {
+      flat = flatten(al, g, i);
+    }
+    for (size_t k = k0; k < chain.size(); ++k) flat = chain[k].apply(al, unflatten(al, chain[k].dims(), flat));
     return flat;
   }
   // Figure 5 inv: reverse application order, O.inv then flatten over O.dims;
@@ -202,7 +213,9 @@ struct Layout {
       std::vector<typename A::V> i = unflatten(al, en, x);
       return expand_inner->inv(al, flatten(al, ne, i));
     }
-    for (size_t k = chain.size(); k-- > 0;) x = flatten(al, chain[k].dims(), chain[k].inv(al, x));
+    const bool direct0 = !chain.empty() && chain[0].dims() == g;
+    for (size_t k = chain.size(); k-- > (direct0 ? 1 : 0);) x = flatten(al, chain[k].dims(), chain[k].inv(al, x));
+    if (direct0) return chain[0].inv(al, x);
     return unflatten(al, g, x);
   }
 };

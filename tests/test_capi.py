@@ -47,7 +47,7 @@ def test_version_and_last_error(lego):
     (lambda L: L.as_layout(L.Row(4, 4)).apply([4, 0]), "OUT_OF_RANGE"),
     (lambda L: L.as_layout(L.Row(4, 4)).inv(16), "OUT_OF_RANGE"),
     (lambda L: L.ExpandBy([5, 7], [6, 9], L.TileOrderBy(L.Row(3, 2), L.Row(2, 4))), "SIZE_MISMATCH"),
-    (lambda L: L.gemm_plan(100, 64, 64, "f16"), "UNSUPPORTED"),
+    (lambda L: L.gemm_plan(64, 64, 64, "f16", bm=64, bn=64, bk=32, wm=48, wn=32), "UNSUPPORTED"),
     (lambda L: L.gemm_plan(64, 64, 64, "f32"), "INVALID_ARG"),
     (lambda L: L.gemm_plan(256, 256, 256, "f16", a=L.as_layout(L.Row(128, 256))), "SIZE_MISMATCH"),
     (lambda L: L.remap_plan(L.as_layout(L.Row(4, 4)), L.as_layout(L.Row(2, 8)), 4), "SIZE_MISMATCH"),

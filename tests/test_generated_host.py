@@ -141,6 +141,9 @@ int main() {
     for (u64 tm = 0; tm < GEMM_MT; ++tm) for (u64 kt = 0; kt < KT; ++kt)
       for (u64 tid = 0; tid < NT; ++tid) for (u64 u = 0; u < A_NV; ++u) {
         if (A_GUARD && u * NT + tid >= A_NVEC) continue;
+#if A_EDGE
+        if (!a_ok((IDX_T)tm, (IDX_T)kt, (IDX_T)tid, (IDX_T)u)) continue;  // padding, read as zero
+#endif
         u64 o = goff_a(tm, kt, tid, u);
         if (o % A_V || o + A_V > GEMM_M * GEMM_K) FAIL("A offset out of range");
         for (int e = 0; e < A_V; ++e) if (a[o + e]++) FAIL("A element loaded twice");
@@ -152,6 +155,9 @@ int main() {
     for (u64 tn = 0; tn < GEMM_NT; ++tn) for (u64 kt = 0; kt < KT; ++kt)
       for (u64 tid = 0; tid < NT; ++tid) for (u64 u = 0; u < B_NV; ++u) {
         if (B_GUARD && u * NT + tid >= B_NVEC) continue;
+#if B_EDGE
+        if (!b_ok((IDX_T)tn, (IDX_T)kt, (IDX_T)tid, (IDX_T)u)) continue;
+#endif
         u64 o = goff_b(tn, kt, tid, u);
         if (o % B_V || o + B_V > GEMM_K * GEMM_N) FAIL("B offset out of range");
         for (int e = 0; e < B_V; ++e) if (b[o + e]++) FAIL("B element loaded twice");
@@ -227,6 +233,9 @@ int main() {
     for (u64 tm = 0; tm < GEMM_MT; ++tm) for (u64 tn = 0; tn < GEMM_NT; ++tn)
       for (u64 lane = 0; lane < 64; ++lane) for (u64 w = 0; w < NWAVES; ++w)
         for (u64 mi = 0; mi < MI; ++mi) for (u64 ni = 0; ni < NI; ++ni) for (u64 r = 0; r < (MB == 32 ? 16 : 4); ++r) {
+#if C_EDGE
+          if (!c_ok((IDX_T)tm, (IDX_T)tn, (IDX_T)lane, (IDX_T)w, (IDX_T)mi, (IDX_T)ni, (IDX_T)r)) continue;
+#endif
 #if C_SEP
           u64 o = (u64)c_t((IDX_T)tm, (IDX_T)tn) + (u64)c_l((IDX_T)lane, (IDX_T)w, (IDX_T)mi, (IDX_T)ni, (IDX_T)r);
 #else
@@ -379,10 +388,12 @@ def _gemm_cases():
     for la, lb in (("Row", "Row"), ("Col", "Row"), ("Col", "Col")):  # m/n-contiguous operands, default plan
         cases.append(dict(M=2048, N=2048, K=2048, dtype="f16", a=L.as_layout(getattr(L, la)(2048, 2048)),
                           b=L.as_layout(getattr(L, lb)(2048, 2048))))
+    from tests.test_gpu_gemm import _ragged_cases
+    cases += _ragged_cases(L)
     return cases
 
 
-@pytest.mark.parametrize("i", range(16))
+@pytest.mark.parametrize("i", range(24))
 def test_gemm_sources_of_gpu_cases(i):
     import paper_2505_08091_amd as L
     cases = _gemm_cases()

@@ -150,7 +150,7 @@ def test_gemm_errors(lego):
     a = torch.zeros(100 * 64, dtype=torch.float16, device=dev)
     c = torch.zeros(100 * 64, dtype=torch.float32, device=dev)
     with pytest.raises(lego.LegoError) as e:
-        lego.gemm(a, a, c, 100, 64, 64, "f16")  # 100 not a multiple of the tile
+        lego.gemm(a, a, c, 64, 64, 64, "f16", wm=48)  # wave tile not a multiple of the MFMA block
     assert e.value.status == "UNSUPPORTED"
     with pytest.raises(lego.LegoError) as e:
         lego.gemm(a, a, c, 64, 64, 64, "f32")
@@ -172,5 +172,41 @@ def test_gemm_mn_contiguous_operands_2048(lego, la_name, lb_name):
     c = _run(lego, a, b, M, N, K, "f16", **kw).reshape(M, N)
     r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(getattr(OL, la_name)(M, K)),
                 OL.as_layout(getattr(OL, lb_name)(K, N)), "f16")
+    ok, mre, fre = OG.check_tolerance(c, r)
+    assert ok, (mre, fre)
+
+
+def _ragged_cases(L):
+    """Sizes the tiles do not divide (partial tiles, Section III-D): padded
+    loads read zero, stores outside C are dropped; includes a ragged last
+    group of the grouped schedule (9 tile rows, groups of 8), a K tail that
+    is not a multiple of the 16-byte vector, and transposed-operand layouts."""
+    return [
+        dict(M=1000, N=1000, K=1000, dtype="bf16"),
+        dict(M=513, N=257, K=320, dtype="f16"),
+        dict(M=100, N=200, K=64, dtype="f16"),
+        dict(M=64, N=64, K=36, dtype="f16"),
+        dict(M=2100, N=300, K=136, dtype="bf16"),
+        dict(M=1000, N=1000, K=1000, dtype="f16", a=L.as_layout(L.Col(1000, 1000)), b=L.as_layout(L.Row(1000, 1000))),
+        dict(M=77, N=1, K=5, dtype="f16"),
+        dict(M=1, N=1, K=1, dtype="bf16"),
+    ]
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_gemm_ragged_sizes(lego, i):
+    """Every output element of a GEMM with partial tiles against the oracle;
+    C is pre-filled with NaN so a dropped or misplaced store shows."""
+    kw = dict(_ragged_cases(lego)[i])
+    M, N, K, dtype = kw.pop("M"), kw.pop("N"), kw.pop("K"), kw.pop("dtype")
+    a = S.tensor(M * K, dtype, seed=S.SEED_A)
+    b = S.tensor(K * N, dtype, seed=S.SEED_B)
+    say(f"gemm ragged {M}x{N}x{K} {dtype} plan={lego.gemm_plan(M, N, K, dtype, **kw)}")
+    c = _run(lego, a, b, M, N, K, dtype, **kw).reshape(M, N)
+    la = kw["a"] if "a" in kw else None
+    ola = OL.as_layout(OL.Col(M, K)) if la is not None else OL.as_layout(OL.Row(M, K))
+    olb = OL.as_layout(OL.Row(K, N)) if "b" in kw else OL.as_layout(OL.Col(K, N))
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), ola, olb, dtype)
+    assert np.isfinite(c).all()
     ok, mre, fre = OG.check_tolerance(c, r)
     assert ok, (mre, fre)
