@@ -257,8 +257,9 @@ def bench_extra(L, reps=20):
     """The other measured workloads: transposing remaps (Row <-> Col fp32,
     the 2D transpose of Section V-C), Row <-> Morton fp16 4096^2 hot and with
     the last-level cache flushed, the 4096^3 fp16 GEMM with A in Morton order
-    and B row-major, and the four Row/Col operand layouts of an 8192^3 fp16
-    GEMM (Section V-A)."""
+    and B row-major, the four Row/Col operand layouts of an 8192^3 fp16 GEMM
+    (Section V-A), and partial tiles: a padding/cropping remap and an 8000^3
+    GEMM (Section III-D)."""
     import torch
     import synth_inputs as S
 
@@ -316,6 +317,32 @@ def bench_extra(L, reps=20):
             ms = _gemm_ms(L, a, b, c, n, "f16", 10, **kw)
             var[f"A {la} B {lb}"] = round(2.0 * n ** 3 / (ms * 1e-3) / 1e12, 1)
     out["gemm_operand_layouts_f16_8192_tflops"] = var
+    del a, b, c
+
+    # Partial tiles (ExpandBy, Section III-D): an 8000 x 8000 fp32 array into a
+    # zero-padded 8192 x 8192 blocked buffer and back, and an 8000^3 bf16 GEMM
+    # whose 256-wide tiles overhang the matrices.
+    n, ne = 8000, 8192
+    x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()
+    padded = torch.empty(ne * ne, dtype=torch.float32, device="cuda")
+    z = torch.empty_like(x)
+    src = L.ExpandBy([n, n], [ne, ne], L.as_layout(L.Row(ne, ne)))
+    blk = L.TileOrderBy(L.Col(ne // 64, ne // 64), L.Row(64, 64))
+    f, i = _alternate(L, src, blk, x, padded, z, reps)
+    # bytes the kernels must move: pad reads n^2 and writes ne^2; crop the reverse
+    nb = (n * n + ne * ne) * 4
+    out["pad_crop_f32_8000_in_8192"] = {"bytes_per_launch": nb, "pad_GBps": gbps(nb, f), "crop_GBps": gbps(nb, i),
+                                        "frac_hbm": round(2 * nb / ((f + i) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                        "plan_pad": L.remap_plan(src, blk, 4)["info"],
+                                        "plan_crop": L.remap_plan(blk, src, 4)["info"]}
+    del x, padded, z
+    a = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_A).cuda()
+    b = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_B).cuda()
+    c = torch.empty(n * n, dtype=torch.float32, device="cuda")
+    ms = _gemm_ms(L, a, b, c, n, "bf16", 10)
+    tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    out["gemm_ragged_bf16_8000"] = {"tflops": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
+                                    "plan": L.gemm_plan(n, n, n, "bf16")}
     return out
 
 
