@@ -258,8 +258,9 @@ def bench_extra(L, reps=20):
     the 2D transpose of Section V-C), Row <-> Morton fp16 4096^2 hot and with
     the last-level cache flushed, the 4096^3 fp16 GEMM with A in Morton order
     and B row-major, the four Row/Col operand layouts of an 8192^3 fp16 GEMM
-    (Section V-A), and partial tiles: a padding/cropping remap and an 8000^3
-    GEMM (Section III-D)."""
+    (Section V-A), partial tiles: a padding/cropping remap and an 8000^3
+    GEMM (Section III-D), and user-defined GenPs from expression text: a
+    wavefront tile order and an LDS swizzle (Section III-B)."""
     import torch
     import synth_inputs as S
 
@@ -343,6 +344,42 @@ def bench_extra(L, reps=20):
     tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
     out["gemm_ragged_bf16_8000"] = {"tflops": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
                                     "plan": L.gemm_plan(n, n, n, "bf16")}
+    del a, b, c
+
+    # User-defined GenPs from expression text: an 8192^2 fp32 array whose 64x64
+    # tiles are stored in antidiagonal (wavefront) order, and the 8192^3 bf16
+    # GEMM with its LDS swizzle written as an expression.
+    n, t = 8192, 64
+    q = n // t
+    antidiag = ("i + j < n0 ? i + (i + j) * (i + j + 1) / 2 : n0 * n0 - 1 - ((n0 - 1 - i) + "
+                "(2 * n0 - 2 - i - j) * (2 * n0 - 1 - i - j) / 2)")
+    tri = "(isqrt(8 * {y} + 1) - 1) / 2"
+    row_of = "({y} - " + tri + " * (" + tri + " + 1) / 2)"
+    up, y2 = "x < n0 * (n0 + 1) / 2", "(n0 * n0 - 1 - x)"
+    inv = [f"{up} ? {row_of.format(y='x')} : n0 - 1 - {row_of.format(y=y2)}",
+           f"{up} ? ({tri.format(y='x')} - {row_of.format(y='x')}) : "
+           f"n0 - 1 - ({tri.format(y=y2)} - {row_of.format(y=y2)})"]
+    wave = L.GroupBy([n, n]).OrderBy(L.RegP([q, t, q, t], [1, 3, 2, 4])).OrderBy(
+        L.GenPExpr([q, q], antidiag, inv), L.Row(t, t))
+    row = L.as_layout(L.Row(n, n))
+    x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()
+    y, z = torch.empty_like(x), torch.empty_like(x)
+    f, i = _alternate(L, row, wave, x, y, z, reps)
+    nb = 2 * n * n * 4
+    out["wavefront_tiles_f32_8192"] = {"bytes_per_launch": nb, "row_to_wavefront_GBps": gbps(nb, f),
+                                       "wavefront_to_row_GBps": gbps(nb, i),
+                                       "frac_hbm": round(2 * nb / ((f + i) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                       "plan": L.remap_plan(row, wave, 4)["info"]}
+    del x, y, z
+    a = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_A).cuda()
+    b = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_B).cuda()
+    c = torch.empty(n * n, dtype=torch.float32, device="cuda")
+    sw = L.as_layout(L.GenPExpr([256, 64], "i * 64 + (((j / 8) ^ ((i / 2) % 8)) * 8) + j % 8",
+                                ["x / 64", "(((x % 64) / 8) ^ ((x / 128) % 8)) * 8 + x % 8"]))
+    ms = _gemm_ms(L, a, b, c, n, "bf16", 10, lds_a=sw, lds_b=sw)
+    tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    out["gemm_expression_lds_bf16_8192"] = {"tflops": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
+                                            "plan": L.gemm_plan(n, n, n, "bf16", lds_a=sw, lds_b=sw)}
     return out
 
 

@@ -94,6 +94,26 @@ enum { LEGO_GENP_MORTON = 1, LEGO_GENP_XOR_SWIZZLE = 2, LEGO_GENP_REVERSE = 3, L
 lego_status lego_genp(int kind, int d, const int64_t* dims, const int64_t* params, int nparams,
                       lego_piece_t* out);
 
+/* A user-defined GenP (Section III-B: any bijection f with its inverse) given
+ * as integer expressions, so that it evaluates on the host and lowers to
+ * kernel code like the built-in GenPs (the paper writes f in Python; text is
+ * what crosses a C ABI).  apply_expr: the physical index within the tile as a
+ * function of the coordinates i0..i{d-1} (i, j, k alias the first three);
+ * inv_exprs: d expressions separated by ';', coordinate k as a function of x.
+ * Both may use the tile extents n0..n{d-1}.  Language: integers, + - * and
+ * floor / % by positive constants, << >> by constants, & with a constant mask
+ * 2^k - 1, ^ on non-negative values, < <= > >= == != ! && || (C truth
+ * values, results 0/1), c ? a : b, parentheses, isqrt (exact floor square root), min, max;
+ * C precedence.  The forward result is taken modulo the tile size and inverse
+ * coordinate k modulo n_k (the identity for a bijection, and a range the
+ * lowering can use).  Tiles of at most 2^20 points are checked exhaustively on
+ * construction (NOT_BIJECTIVE when f is not a bijection onto [0, size) or the
+ * inverse does not undo it); larger ones can be checked with
+ * lego_verify_bijective.  Errors: INVALID_ARG (syntax, unsupported operation,
+ * with the offset in lego_last_error), NOT_BIJECTIVE. */
+lego_status lego_genp_expr(int d, const int64_t* dims, const char* apply_expr, const char* inv_exprs,
+                           lego_piece_t* out);
+
 /* Rank and dims of a piece; dims must hold 16 entries. */
 lego_status lego_piece_dims(lego_piece_t p, int* rank, int64_t* dims);
 

@@ -17,5 +17,6 @@ Modules
           Morton, XOR swizzle).
   remap   the permutation dst[L_dst.apply(x)] = src[L_src.apply(x)].
   gemm    C = A @ B in fp64 with operands read through layouts.
+  genexpr user-defined GenP pieces written as integer expressions.
 """
-from . import layout, remap, gemm  # noqa: F401
+from . import layout, remap, gemm, genexpr  # noqa: F401

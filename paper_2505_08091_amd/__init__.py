@@ -56,6 +56,7 @@ _SIGS = {
     "lego_row": ([ctypes.c_int, c_i64p, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_col": ([ctypes.c_int, c_i64p, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_genp": ([ctypes.c_int, ctypes.c_int, c_i64p, c_i64p, ctypes.c_int, ctypes.POINTER(_vp)], ctypes.c_int),
+    "lego_genp_expr": ([ctypes.c_int, c_i64p, ctypes.c_char_p, ctypes.c_char_p, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_piece_dims": ([_vp, ctypes.POINTER(ctypes.c_int), c_i64p], ctypes.c_int),
     "lego_groupby": ([ctypes.c_int, c_i64p, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_orderby": ([_vp, ctypes.c_int, ctypes.POINTER(_vp), ctypes.POINTER(_vp)], ctypes.c_int),
@@ -175,6 +176,19 @@ def GenP(kind, dims, params=()):  # noqa: N802
     return Piece(out)
 
 
+def GenPExpr(dims, apply, inv):  # noqa: N802
+    """A user-defined GenP from integer expressions (grammar in include/lego.h):
+    ``apply`` over i0..i{d-1} (or i, j, k), ``inv`` one expression per
+    dimension over x."""
+    if isinstance(inv, str) or len(inv) != len(dims):
+        raise LegoError(-1, "inv must hold one expression per dimension")
+    if any(";" in t for t in inv):
+        raise LegoError(-1, "';' separates the inverse expressions")
+    out = ctypes.c_void_p()
+    _check(_lib.lego_genp_expr(len(dims), _i64(dims), apply.encode(), ";".join(inv).encode(), ctypes.byref(out)))
+    return Piece(out)
+
+
 def _dims(d):
     if len(d) == 1 and isinstance(d[0], (list, tuple)):
         return [int(x) for x in d[0]]
@@ -285,11 +299,13 @@ def mfma_fragment_layout(instr, operand):
 # ------------------------------------------------------------------ device --
 def apply_all_device(layout, out, stream=None):
     """out[x] = apply(x) for every logical flat x (out: int32/int64 cuda tensor)."""
+    _need(out, layout.size(), "output")
     _check(_lib.lego_apply_all_device(layout.h, out.element_size(), _ptr(out), _stream(stream)))
 
 
 def inv_all_device(layout, out, stream=None):
     """out[p, k] = inv(p)[k] for every physical p (out: [N, rank] int32/int64)."""
+    _need(out, layout.phys_size() * layout.rank(), "output")
     _check(_lib.lego_inv_all_device(layout.h, out.element_size(), _ptr(out), _stream(stream)))
 
 

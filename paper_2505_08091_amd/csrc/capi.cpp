@@ -200,6 +200,26 @@ lego_status lego_genp(int kind, int d, const int64_t* dims, const int64_t* param
   });
 }
 
+lego_status lego_genp_expr(int d, const int64_t* dims, const char* apply_expr, const char* inv_exprs,
+                           lego_piece_t* out) {
+  return guard([&] {
+    auto n = dims_arg(d, dims);
+    if (!apply_expr || !inv_exprs) throw std::invalid_argument("null expression");
+    std::vector<std::string> inv;
+    std::string cur;
+    for (const char* c = inv_exprs;; ++c) {
+      if (*c == ';' || *c == 0) {
+        inv.push_back(cur);
+        cur.clear();
+        if (!*c) break;
+      } else {
+        cur += *c;
+      }
+    }
+    return out_piece(make_genp_expr(n, apply_expr, inv), out);
+  });
+}
+
 lego_status lego_piece_dims(lego_piece_t p, int* rank, int64_t* dims) {
   return guard([&] {
     auto pc = piece_of(p);

@@ -7,6 +7,8 @@
 //   LEGO_FN IDX_T src_vec(IDX_T t)   source vector index of destination vector t
 //   LEGO_FN IDX_T blk(IDX_T b)       destination chunk of schedule position b
 //   NBLK                             number of chunks
+//   SRC_SEP, LEGO_FN IDX_T src_base(IDX_T c), src_loc(IDX_T r)   1: the source
+//                                    vector of chunk c's vector r is src_base(c) + src_loc(r)
 //   MASKED, LEGO_FN IDX_T src_ok(IDX_T t)   1: vector t has a source (an
 //                                    ExpandBy source, Figure 9); else it is zero
 // LDS path (both sides are digit permutations; a tile of TILE elements is read
@@ -35,16 +37,24 @@ typedef ELEM_T vec_t __attribute__((ext_vector_type(V)));
 // thread, then UNROLL stores.
 LEGO_FN void remap_chunk(const vec_t* __restrict__ src, vec_t* __restrict__ dst, u64 c) {
   const u64 base = c * (NT * UNROLL) + threadIdx.x;
+#if SRC_SEP
+  // chunk part of the map, once per workgroup (c is uniform)
+  const vec_t* __restrict__ sc = src + src_base((IDX_T)c);
+#define SRC_OF(t, u) (sc + src_loc((IDX_T)((u64)(u) * NT + threadIdx.x)))
+#else
+#define SRC_OF(t, u) (src + src_vec((IDX_T)(t)))
+#endif
   vec_t v[UNROLL];
 #pragma unroll
   for (int u = 0; u < UNROLL; ++u) {
     const u64 t = base + (u64)u * NT;
 #if MASKED
-    if (t < NVEC) v[u] = src_ok((IDX_T)t) ? LEGO_LD(src + src_vec((IDX_T)t)) : (vec_t){};
+    if (t < NVEC) v[u] = src_ok((IDX_T)t) ? LEGO_LD(SRC_OF(t, u)) : (vec_t){};
 #else
-    if (t < NVEC) v[u] = LEGO_LD(src + src_vec((IDX_T)t));
+    if (t < NVEC) v[u] = LEGO_LD(SRC_OF(t, u));
 #endif
   }
+#undef SRC_OF
 #pragma unroll
   for (int u = 0; u < UNROLL; ++u) {
     const u64 t = base + (u64)u * NT;

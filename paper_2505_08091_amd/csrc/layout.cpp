@@ -3,7 +3,10 @@
 // Equation (2)).
 #include "layout.hpp"
 
+#include "errors.hpp"
+
 #include <algorithm>
+#include <functional>
 #include <sstream>
 
 namespace lego {
@@ -74,10 +77,14 @@ std::string Piece::describe() const {
     vec(sigma);
     o << ")";
   } else {
-    static const char* names[] = {"?", "morton", "xor_swizzle", "reverse", "antidiag"};
+    static const char* names[] = {"?", "morton", "xor_swizzle", "reverse", "antidiag", "expr"};
     o << "GenP(";
     vec(n);
     o << "," << names[gk];
+    if (gk == GEN_EXPR) {
+      o << ",\"" << ex->apply_text << "\"";
+      for (auto& t : ex->inv_text) o << ",\"" << t << "\"";
+    }
     if (!prm.empty()) {
       o << ",";
       vec(prm);
@@ -145,6 +152,50 @@ PieceP make_genp(int kind, const std::vector<i64>& n, const std::vector<i64>& pr
       break;
     default:
       throw std::invalid_argument("unknown GenP kind");
+  }
+  return p;
+}
+
+PieceP make_genp_expr(const std::vector<i64>& n, const std::string& apply, const std::vector<std::string>& inv) {
+  check_dims(n);
+  const size_t d = n.size();
+  if (inv.size() != d) throw std::invalid_argument("an expression GenP needs one inverse expression per dimension");
+  std::vector<std::pair<std::string, i64>> consts;
+  for (size_t k = 0; k < d; ++k) consts.push_back({"n" + std::to_string(k), n[k]});
+  std::vector<std::string> fwd_vars;
+  for (size_t k = 0; k < d; ++k) fwd_vars.push_back("i" + std::to_string(k));
+  static const char* short_names[] = {"i", "j", "k"};
+  for (size_t k = 0; k < d && k < 3; ++k) fwd_vars.push_back(short_names[k]);
+  auto ex = std::make_shared<GenExpr>();
+  ex->apply_text = apply;
+  ex->inv_text = inv;
+  // the short names alias the first coordinates: map them onto i0..i2
+  GNodeP fwd = parse_gexpr(apply, fwd_vars, consts);
+  std::function<GNodeP(const GNodeP&)> alias = [&](const GNodeP& g) -> GNodeP {
+    auto c = std::make_shared<GNode>(*g);
+    if (c->k == GNode::Var && c->var >= (int)d) c->var -= (int)d;
+    for (auto& kid : c->kids) kid = alias(kid);
+    return c;
+  };
+  ex->apply = alias(fwd);
+  for (auto& t : inv) ex->inv.push_back(parse_gexpr(t, {"x"}, consts));
+  auto p = std::make_shared<Piece>();
+  p->regp = false;
+  p->gk = GEN_EXPR;
+  p->n = n;
+  p->ex = ex;
+  // Small tiles are checked exhaustively: f must be a bijection onto
+  // [0, |tile|) and the inverse must undo it.
+  const i64 N = product(n);
+  if (N <= (i64(1) << 20)) {
+    IntAlg al;
+    std::vector<char> hit(N, 0);
+    for (i64 x = 0; x < N; ++x) {
+      std::vector<i64> i = unflatten(al, n, x);
+      i64 f = p->apply(al, i);
+      if (f < 0 || f >= N || hit[f]++) throw NotBijective("the expression GenP is not a bijection onto [0, size)");
+      if (p->inv(al, f) != i) throw NotBijective("the inverse expressions do not invert the forward map");
+    }
   }
   return p;
 }

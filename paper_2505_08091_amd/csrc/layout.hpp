@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "expr.hpp"
+#include "genexpr.hpp"
 
 namespace lego {
 
@@ -89,7 +90,7 @@ std::vector<int> sigma_dq(int d, int q);
 i64 product(const std::vector<i64>& v);
 
 // ------------------------------------------------------------- permutations
-enum GenKind { GEN_MORTON = 1, GEN_XOR_SWIZZLE = 2, GEN_REVERSE = 3, GEN_ANTIDIAG = 4 };
+enum GenKind { GEN_MORTON = 1, GEN_XOR_SWIZZLE = 2, GEN_REVERSE = 3, GEN_ANTIDIAG = 4, GEN_EXPR = 5 };
 
 struct Piece {
   bool regp = true;
@@ -97,6 +98,7 @@ struct Piece {
   std::vector<int> sigma;  // RegP: 1-based gather permutation
   int gk = 0;              // GenP kind
   std::vector<i64> prm;    // GenP parameters
+  std::shared_ptr<const GenExpr> ex;  // GEN_EXPR: the forward and inverse expressions
 
   i64 size() const { return product(n); }
   std::string describe() const;
@@ -225,6 +227,10 @@ PieceP make_regp(const std::vector<i64>& n, const std::vector<int>& sigma);
 PieceP make_row(const std::vector<i64>& n);
 PieceP make_col(const std::vector<i64>& n);
 PieceP make_genp(int kind, const std::vector<i64>& n, const std::vector<i64>& prm);
+// GenP from expression text (grammar in genexpr.hpp): the forward map over
+// i0..i{d-1} and one inverse expression per dimension over x.  Tiles of at most
+// 2^20 points are checked exhaustively (NotBijective on failure).
+PieceP make_genp_expr(const std::vector<i64>& n, const std::string& apply, const std::vector<std::string>& inv);
 LayoutP make_groupby(const std::vector<i64>& dims);
 LayoutP make_orderby(const LayoutP& base, const std::vector<PieceP>& pieces);
 LayoutP make_tileby(int q, int d, const std::vector<i64>& tiles);
@@ -266,6 +272,10 @@ typename A::V Piece::genp_apply(const A& al, const std::vector<typename A::V>& i
       for (size_t k = 0; k < n.size(); ++k) r.push_back(al.sub(al.c(n[k] - 1), i[k]));
       return flatten(al, n, r);
     }
+    case GEN_EXPR:
+      // Taken modulo the tile size: the identity on a bijection onto
+      // [0, size), and it tells the lowering the range of the result.
+      return al.mod(eval_gexpr(al, *ex->apply, i), size());
     case GEN_ANTIDIAG: {
       // Figure 7: order of the 2n-1 antidiagonals, top row first.
       i64 nn = n[0];
@@ -303,6 +313,11 @@ std::vector<typename A::V> Piece::genp_inv(const A& al, const typename A::V& x) 
     case GEN_REVERSE: {
       std::vector<V> r = unflatten(al, n, al.sub(al.c(product(n) - 1), x));
       return r;
+    }
+    case GEN_EXPR: {
+      std::vector<V> out;
+      for (size_t k = 0; k < ex->inv.size(); ++k) out.push_back(al.mod(eval_gexpr(al, *ex->inv[k], std::vector<V>{x}), n[k]));
+      return out;
     }
     case GEN_ANTIDIAG: {
       // Figure 7 inverse with the exact integer square root.

@@ -24,13 +24,16 @@ const char* elem_type(int bytes) {
 std::string header() { return std::string(prelude_text()); }
 
 // Emit every function with one common index type (64-bit if any needs it).
+// Functions named in `parts` are parts of one additive split and all come from
+// the expanded lowering (the form the split was proven on).
 std::string emit_all(std::vector<std::pair<std::string, std::function<FnSpec(Ctx&)>>> fns, bool* wide_out,
-                     std::string* info) {
+                     std::string* info, const std::vector<std::string>& parts = {}) {
+  auto variant = [&](const std::string& n) { return std::find(parts.begin(), parts.end(), n) != parts.end() ? 0 : -1; };
   bool wide = false;
-  for (auto& f : fns) wide = wide || emit_best(f.first, f.second).wide;
+  for (auto& f : fns) wide = wide || emit_best(f.first, f.second, false, variant(f.first)).wide;
   std::string code;
   for (auto& f : fns) {
-    Emitted e = emit_best(f.first, f.second, wide);
+    Emitted e = emit_best(f.first, f.second, wide, variant(f.first));
     code += e.code;
     if (info) *info += " " + f.first + ":" + std::to_string(e.ops) + "ops";
   }
@@ -223,8 +226,36 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     // vectors): measured ahead of 2, 4 and 16, and of 128/512/1024 threads.
     int NT = 256, UNROLL = 8;
     if (const char* e = std::getenv("LEGO_REMAP_NT")) NT = std::atoi(e);
-    if (const char* e = std::getenv("LEGO_REMAP_UNROLL")) UNROLL = std::atoi(e);
+    const char* unroll_env = std::getenv("LEGO_REMAP_UNROLL");
+    if (unroll_env) UNROLL = std::atoi(unroll_env);
     const i64 nvec = N / V;
+    // Source vector of destination vector t, as an expression of t.
+    auto src_vec_of = [&](Ctx& c, const Sum& t) {
+      int pv = c.var("p", N);
+      Sum vv;
+      return fdiv(c, subst(c, remap_map_masked(c, src, dst, pv, &vv), pv, mulc(c, t, V)), V);
+    };
+    // A map that is not a digit permutation (a GenP, ExpandBy, ...) can cost
+    // far more than a vector copy per vector.  When the map splits additively
+    // into a chunk part and an in-chunk part, the chunk part is computed once
+    // per workgroup: take the largest chunk (8, 4, 2 or 1 vectors per thread)
+    // for which it does.
+    bool src_sep = false;
+    if (!pure) {
+      for (int u : {8, 4, 2, 1}) {
+        if (unroll_env && u != UNROLL) continue;
+        const i64 ch = (i64)NT * u;
+        if (nvec % ch) continue;
+        Ctx c;
+        int cb = c.var("c", nvec / ch), r = c.var("r", ch);
+        Sum F, G;
+        if (split_by(src_vec_of(c, add(c, mulc(c, var(c, cb), ch), var(c, r))), {cb}, &F, &G)) {
+          UNROLL = u;
+          src_sep = true;
+          break;
+        }
+      }
+    }
     const i64 chunk = (i64)NT * UNROLL;
     const i64 nblk = (nvec + chunk - 1) / chunk;
     // Chunk order.  For a digit map whose chunks are whole digits, the
@@ -281,6 +312,20 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
                                    f.outs = {fdiv(c, m, V)};
                                    return f;
                                  }}};
+    // (declared at this scope: the builders run later, inside emit_all)
+    auto part = [&](Ctx& c, bool base) {
+      int cb = c.var("c", nblk), r = c.var("r", chunk);
+      Sum F, G;
+      FnSpec f;
+      f.valid = split_by(src_vec_of(c, add(c, mulc(c, var(c, cb), chunk), var(c, r))), {cb}, &F, &G);
+      f.params = {base ? cb : r};
+      f.outs = {base ? F : G};
+      return f;
+    };
+    if (src_sep) {
+      dfns.push_back({"src_base", [&](Ctx& c) { return part(c, true); }});
+      dfns.push_back({"src_loc", [&](Ctx& c) { return part(c, false); }});
+    }
     if (masked)
       dfns.push_back({"src_ok", [&](Ctx& c) {
                         int t = c.var("t", nvec);
@@ -292,8 +337,9 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
                         f.outs = {subst(c, vv, pv, mulc(c, var(c, t), V))};
                         return f;
                       }});
-    std::string fns = emit_all(dfns, &wide, &info);
+    std::string fns = emit_all(dfns, &wide, &info, {"src_base", "src_loc"});
     s << header() << "#define ELEM_T " << et << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define V " << V
+      << "\n#define SRC_SEP " << (src_sep ? 1 : 0)
       << "\n#define NVEC " << nvec << "ull\n#define NBLK " << nblk << "ull\n#define NT " << NT << "\n#define UNROLL " << UNROLL
       << "\n#define NONTEMPORAL " << nontemporal << "\n#define MASKED " << (masked ? 1 : 0) << "\n#define NSRC " << NS
       << "ull\n#define LEGO_REMAP_DIRECT 1\n"
@@ -309,6 +355,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     R.src = s.str();
     R.info = std::string(R.path == REMAP_DIRECT ? "direct" : "gather") + (src_order ? " src-order" : " dst-order") +
              " NT=" + std::to_string(NT) + " UNROLL=" + std::to_string(UNROLL) + " V=" + std::to_string(V) +
+             (src_sep ? " chunk-base" : "") +
              " run=" + std::to_string(run) + (masked ? " masked" : "") + info;
     return R;
   }

@@ -176,3 +176,57 @@ def test_binding_checks_buffer_sizes_before_launch(lego):
         lego.gemm(torch.zeros(64 * 64, dtype=torch.float16), torch.zeros(64 * 63, dtype=torch.float16),
                   torch.zeros(64 * 64), 64, 64, 64, "f16")
     assert err.value.status == "SIZE_MISMATCH"
+
+
+def _all_points(lay):
+    dims = lay.dims()
+    return [list(p) for p in np.ndindex(*dims)]
+
+
+def test_expression_genp_host_matches_oracle(lego):
+    """GenPs from expression text evaluate on the host exactly as the oracle's
+    independent evaluator of the same text, forward and inverse."""
+    from oracle import genexpr as GX
+    from tests import genp_exprs as GE
+    cases = [([6, 6], GE.ANTIDIAG_APPLY, GE.ANTIDIAG_INV), ([8, 8], GE.MORTON8_APPLY, GE.MORTON8_INV),
+             ([32, 64], GE.SWIZZLE64_APPLY, GE.SWIZZLE64_INV),
+             ([3, 4, 5], "(i2 * n1 + i1) * n0 + i0", ["x % n0", "(x / n0) % n1", "x / (n0 * n1)"])]
+    for dims, fwd, inv in cases:
+        lay = lego.as_layout(lego.GenPExpr(dims, fwd, inv))
+        ref = OL.as_layout(GX.expr_genp(dims, fwd, inv))
+        for p in _all_points(lay):
+            f = lay.apply(p)
+            assert f == int(ref.apply(p))
+            assert lay.inv(f) == [int(v) for v in ref.inv(f)]
+    # in a chain, as a per-tile order (antidiagonal order of 2x2 tiles)
+    lay = lego.GroupBy([6, 6]).OrderBy(lego.RegP([3, 2, 3, 2], [1, 3, 2, 4])).OrderBy(
+        lego.GenPExpr([3, 3], GE.ANTIDIAG_APPLY, GE.ANTIDIAG_INV), lego.Row(2, 2))
+    ref = OL.GroupBy([6, 6]).OrderBy(OL.RegP([3, 2, 3, 2], [1, 3, 2, 4])).OrderBy(OL.antidiag_genp(3), OL.Row(2, 2))
+    for p in _all_points(lay):
+        assert lay.apply(p) == int(ref.apply(p))
+
+
+@pytest.mark.parametrize("fwd,inv,status", [
+    ("i * n1 + j +", ["x / n1", "x % n1"], "INVALID_ARG"),         # syntax
+    ("i * n1 + j", ["x / j", "x % n1"], "INVALID_ARG"),            # unknown name / non-constant divisor
+    ("i * n1 + (j & 6)", ["x / n1", "x % n1"], "INVALID_ARG"),     # mask not 2^k - 1
+    ("0", ["x / n1", "x % n1"], "NOT_BIJECTIVE"),                   # not a bijection
+    ("i * n1 + j", ["x % n1", "x / n1"], "NOT_BIJECTIVE"),          # inverse does not invert
+    ("i * n1 + j", ["x / n1"], "INVALID_ARG"),                      # one inverse per dimension
+])
+def test_expression_genp_errors(lego, fwd, inv, status):
+    with pytest.raises(lego.LegoError) as e:
+        lego.GenPExpr([4, 5], fwd, inv)
+    assert e.value.status == status
+
+
+@pytest.mark.parametrize("text,value", [
+    ("1 + 2 * 3 << 1", 14), ("5 - 3 - 1", 1), ("2 ^ 3 & 1", 3), ("0 - 7 / 2", -3), ("-7 / 2", -4),
+    ("-7 % 2", 1), ("1 < 2 == 1", 1), ("0 ? 5 : 1 ? 6 : 7", 6), ("isqrt(99)", 9), ("isqrt(100)", 10),
+    ("max(3, min(9, 4))", 4), ("!0 + !5", 1), ("1 && 0 || 1", 1), ("3 >= 3 && 2 > 3", 0), ("6 != 6", 0),
+])
+def test_expression_language_host(lego, text, value):
+    """The library's parser on the same hand-worked values as the oracle's:
+    a shift of a 1009-point tile by the expression's value exposes it."""
+    g = lego.as_layout(lego.GenPExpr([1009], f"i + ({text})", [f"x - ({text})"]))
+    assert g.apply([0]) == value % 1009

@@ -319,8 +319,9 @@ def test_generated_source_on_host(i):
 # Every configuration the GPU tests launch, checked on the host first.
 def _index_cases():
     import paper_2505_08091_amd as L
+    from tests.test_gpu_genexpr import _wavefront
     from tests.test_gpu_index import _cases
-    return _cases(L)
+    return _cases(L) + [("wavefront 1024^2 of 32x32 tiles", _wavefront(L, None, 1024, 32), _wavefront(None, OL, 1024, 32))]
 
 
 def test_index_sources_of_gpu_cases():
@@ -340,8 +341,9 @@ def test_index_sources_of_gpu_cases():
 
 def _remap_cases():
     import paper_2505_08091_amd as L
+    from tests.test_gpu_genexpr import _expr_cases
     from tests.test_gpu_remap import _expand_cases, _small_cases
-    cases = [(n, ls, ld, ols, old) for n, ls, ld, ols, old in _small_cases(L) + _expand_cases(L)]
+    cases = [(n, ls, ld, ols, old) for n, ls, ld, ols, old in _small_cases(L) + _expand_cases(L) + _expr_cases(L)]
     for n in (2048, 4096, 1024):
         cases.append((f"transpose {n}", L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n)),
                       OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.Col(n, n))))
@@ -390,10 +392,13 @@ def _gemm_cases():
                           b=L.as_layout(getattr(L, lb)(2048, 2048))))
     from tests.test_gpu_gemm import _ragged_cases
     cases += _ragged_cases(L)
+    from tests import genp_exprs as GE
+    sw = L.as_layout(L.GenPExpr([256, 64], GE.SWIZZLE64_APPLY, GE.SWIZZLE64_INV))
+    cases.append(dict(M=1024, N=1024, K=1024, dtype="bf16", lds_a=sw, lds_b=sw))
     return cases
 
 
-@pytest.mark.parametrize("i", range(24))
+@pytest.mark.parametrize("i", range(25))
 def test_gemm_sources_of_gpu_cases(i):
     import paper_2505_08091_amd as L
     cases = _gemm_cases()

@@ -533,3 +533,49 @@ def test_planted_transposed_gemm_operand_is_caught():
     # B stored row-major but described as Col: the product must differ
     r = G.gemm(_f16(a.ravel()), _f16(b.ravel()), L.as_layout(L.Row(m, m)), L.as_layout(L.Col(m, m)), "f16")
     assert not (r == a @ b).all()
+
+
+# ------------------------------------------------- expression GenP (oracle)
+from oracle import genexpr as GX  # noqa: E402
+from tests import genp_exprs as GE  # noqa: E402
+
+
+@pytest.mark.parametrize("text,value", [
+    ("1 + 2 * 3 << 1", 14), ("5 - 3 - 1", 1), ("2 ^ 3 & 1", 3), ("0 - 7 / 2", -3), ("-7 / 2", -4),
+    ("-7 % 2", 1), ("1 < 2 == 1", 1), ("0 ? 5 : 1 ? 6 : 7", 6), ("isqrt(99)", 9), ("isqrt(100)", 10),
+    ("max(3, min(9, 4))", 4), ("!0 + !5", 1), ("1 && 0 || 1", 1), ("3 >= 3 && 2 > 3", 0), ("6 != 6", 0),
+])
+def test_expression_language_follows_c_rules(text, value):
+    """Precedence, associativity and floor division of the expression
+    language, on values worked out by hand from C's rules."""
+    assert int(GX.evaluate(text)) == value
+
+
+def test_expression_antidiag_equals_figure7():
+    """The antidiagonal order written as an expression equals the Figure 7
+    permutation (pinned above) for n = 1..12, forward and inverse."""
+    for n in range(1, 13):
+        g = GX.expr_genp([n, n], GE.ANTIDIAG_APPLY, GE.ANTIDIAG_INV)
+        ref = L.antidiag_genp(n)
+        i, j = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+        assert (g.apply([i, j]) == ref.apply([i, j])).all()
+        x = np.arange(n * n)
+        assert all((a == b).all() for a, b in zip(g.inv(x), ref.inv(x)))
+
+
+def test_expression_morton_and_row_col():
+    """Bit-level Z order equals GenP(morton) on 8x8; i*n1+j and j*n0+i equal
+    Row and Col."""
+    i, j = np.meshgrid(np.arange(8), np.arange(8), indexing="ij")
+    g = GX.expr_genp([8, 8], GE.MORTON8_APPLY, GE.MORTON8_INV)
+    assert (g.apply([i, j]) == L.morton_genp(8, 8).apply([i, j])).all()
+    x = np.arange(64)
+    assert all((a == b).all() for a, b in zip(g.inv(x), L.morton_genp(8, 8).inv(x)))
+    i, j = np.meshgrid(np.arange(5), np.arange(7), indexing="ij")
+    row = GX.expr_genp([5, 7], "i * n1 + j", ["x / n1", "x % n1"])
+    col = GX.expr_genp([5, 7], "i1 * n0 + i0", ["x % n0", "x / n0"])
+    assert (row.apply([i, j]) == L.Row(5, 7).apply([i, j])).all()
+    assert (col.apply([i, j]) == L.Col(5, 7).apply([i, j])).all()
+    s = GX.expr_genp([256, 64], GE.SWIZZLE64_APPLY, GE.SWIZZLE64_INV)
+    i, j = np.meshgrid(np.arange(256), np.arange(64), indexing="ij")
+    assert (s.apply([i, j]) == L.xor_swizzle_genp(256, 64, 8, 2).apply([i, j])).all()
