@@ -107,6 +107,11 @@ struct Operand {
   bool is_b;
   int V = 1, axis = 1, NV = 1;
   int gaxis = 1;  // axis of the widest contiguous global vector (reported)
+  // axis 2: a load vector is a VR x VC block of the tile whose V = VR * VC
+  // elements are contiguous in global memory in the order given per bit of the
+  // element index e: bit b moves by (bdi[b], bdj[b]) (e.g. 2 x 4 blocks of Z order).
+  int VR = 1, VC = 1;
+  std::vector<i64> bdi, bdj;
   i64 NVEC = 0;
   bool guard = false, sep = false, svec = false, frvec = false;
   bool frtr = false;      // fragments read with the transposing LDS load
@@ -223,7 +228,17 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       *j = ij[1];
       return;
     }
-    if (o.axis == 1) {
+    if (o.axis == 2) {
+      i64 per = o.KD / o.VC;
+      Sum di = cst(0), dj = cst(0);
+      for (size_t b = 0; b < o.bdi.size(); ++b) {
+        Sum bit = fmod(c, fdiv(c, e, i64(1) << b), 2);
+        di = add(c, di, mulc(c, bit, o.bdi[b]));
+        dj = add(c, dj, mulc(c, bit, o.bdj[b]));
+      }
+      *i = add(c, mulc(c, fdiv(c, q, per), o.VR), di);
+      *j = add(c, mulc(c, fmod(c, q, per), o.VC), dj);
+    } else if (o.axis == 1) {
       i64 per = o.KD / o.V;
       *i = fdiv(c, q, per);
       *j = add(c, mulc(c, fmod(c, q, per), o.V), e);
@@ -262,6 +277,56 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       }
       if (found) break;
     }
+    // No 16-byte run along one axis: try 8 elements contiguous in global memory
+    // that form a small 2D block of the tile (Z order keeps 2 x 4 blocks together).
+    if (o.V < 8) {
+      for (auto shape : {std::pair<int, int>{2, 4}, {4, 2}}) {
+        const int vr = shape.first, vc = shape.second;
+        if (o.R % vr || o.KD % vc) continue;
+        // The order of the 8 elements, read off the layout at the origin.
+        IntAlg ia;
+        const i64 g0 = o.is_b ? o.glob->apply(ia, {0, 0}) : o.glob->apply(ia, {0, 0});
+        std::vector<i64> di(8), dj(8);
+        bool ok = true;
+        for (int e = 0; e < 8 && ok; ++e) {
+          if (g0 + e >= o.glob->phys_size()) {
+            ok = false;
+            break;
+          }
+          std::vector<i64> lc = o.glob->inv(ia, g0 + e);
+          di[e] = o.is_b ? lc[1] : lc[0];
+          dj[e] = o.is_b ? lc[0] : lc[1];
+          ok = di[e] >= 0 && di[e] < vr && dj[e] >= 0 && dj[e] < vc;
+        }
+        // linear over the bits of e
+        for (int e = 0; e < 8 && ok; ++e) {
+          i64 si = 0, sj = 0;
+          for (int b = 0; b < 3; ++b)
+            if (e >> b & 1) si += di[1 << b], sj += dj[1 << b];
+          ok = si == di[e] && sj == dj[e];
+        }
+        if (!ok) continue;
+        Operand t = o;
+        t.axis = 2;
+        t.V = 8;
+        t.VR = vr;
+        t.VC = vc;
+        t.bdi = {di[1], di[2], di[4]};
+        t.bdj = {dj[1], dj[2], dj[4]};
+        // every block of every tile: 8 contiguous, aligned elements
+        Ctx c;
+        int tt = c.var("tt", o.is_b ? Nt : Mt), kt = c.var("kt", Kt), q = c.var("q", o.R * o.KD / 8),
+            e = c.var("e", 8);
+        Sum i, j;
+        load_elem(c, t, var(c, q), cst(0), var(c, e), &i, &j);
+        Sum off = glob_off(c, t, var(c, tt), var(c, kt), i, j);
+        Sum okv = in_range(c, t, var(c, tt), var(c, kt), i, j);
+        if (contiguous_in(off, e, 8) && !(o.edge && depends_on(okv, e))) {
+          o = t;
+          break;
+        }
+      }
+    }
     o.gaxis = o.axis;
     // An operand contiguous along m/n keeps that orientation in LDS.
     if (!o.user_lds && o.axis == 0 && o.V >= 4) o.lds = tr_lds(o.R, o.KD);
@@ -286,8 +351,16 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       Sum i, j;
       load_elem(c, o, var(c, tid), var(c, u), var(c, e), &i, &j);
       SymAlg al{&c};
-      o.svec = o.V > 1 && contiguous_in(o.lds->apply(al, {i, j}), e, o.V);
-      if (o.V == 1) o.svec = true;
+      if (o.axis == 2) {
+        // stored one block row at a time: VC elements contiguous in LDS
+        Sum i0, j0;
+        load_elem(c, o, var(c, tid), var(c, u), cst(0), &i0, &j0);
+        int r = c.var("r", o.VR), cc = c.var("cc", o.VC);
+        o.svec = contiguous_in(o.lds->apply(al, {add(c, i0, var(c, r)), add(c, j0, var(c, cc))}), cc, o.VC);
+      } else {
+        o.svec = o.V > 1 && contiguous_in(o.lds->apply(al, {i, j}), e, o.V);
+        if (o.V == 1) o.svec = true;
+      }
     }
     // Vector fragment read?
     {
@@ -626,7 +699,23 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
       << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "FRTR " << (o.frtr ? 1 : 0) << "\n#define " << P2[k]
       << "NVEC " << o.NVEC << "u\n#define " << P2[k]
       << "GUARD " << (o.guard ? 1 : 0) << "\n#define " << P2[k] << "EDGE " << (o.edge ? 1 : 0) << "\n#define "
-      << P2[k] << "BYTES " << 2 * o.glob->phys_size() << "u\n";
+      << P2[k] << "BYTES " << 2 * o.glob->phys_size() << "u\n#define " << P2[k] << "VR " << o.VR << "\n#define "
+      << P2[k] << "VC " << (o.axis == 2 ? o.VC : o.V) << "\n";
+    // Block vectors: element index of block position (r, c), row-major.
+    s << "static constexpr int " << P2[k] << "BIDX[] = {";
+    if (o.axis == 2) {
+      for (int r = 0; r < o.VR; ++r)
+        for (int cc = 0; cc < o.VC; ++cc)
+          for (int e = 0; e < o.V; ++e) {
+            i64 di = 0, dj = 0;
+            for (int b = 0; b < 3; ++b)
+              if (e >> b & 1) di += o.bdi[b], dj += o.bdj[b];
+            if (di == r && dj == cc) s << e << ",";
+          }
+    } else {
+      s << "0";
+    }
+    s << "};\n";
   }
   s << "#define C_EDGE " << (cedge ? 1 : 0) << "\n";
   // Two staging register sets when the accumulators live in AGPRs (one wave
@@ -650,10 +739,12 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   std::ostringstream info;
   info << "gemm " << M << "x" << N << "x" << K << (rq.dtype == LEGO_BF16 ? " bf16" : " f16") << " tile " << bm << "x"
        << bn << "x" << bk << " waves " << NWM << "x" << NWN << " wave " << wm << "x" << wn << " mfma " << MB << "x"
-       << MB << "x" << KB << " sched" << (xcd ? "+xcd" : "") << " A:V" << ops[0].V << (ops[0].gaxis ? "k" : "m")
+       << MB << "x" << KB << " sched" << (xcd ? "+xcd" : "") << " A:V" << ops[0].V
+       << (ops[0].gaxis == 2 ? "b" + std::to_string(ops[0].VR) + "x" + std::to_string(ops[0].VC) : (ops[0].gaxis ? "k" : "m"))
        << (ops[0].sep ? " sep" : " full") << (ops[0].svec ? " svec" : " sscalar")
        << (ops[0].frvec ? " frvec" : (ops[0].frtr ? " frtr" : " frscalar")) << " B:V" << ops[1].V
-       << (ops[1].gaxis ? "k" : "n") << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
+       << (ops[1].gaxis == 2 ? "b" + std::to_string(ops[1].VR) + "x" + std::to_string(ops[1].VC) : (ops[1].gaxis ? "k" : "n"))
+       << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
        << (ops[1].frvec ? " frvec" : (ops[1].frtr ? " frtr" : " frscalar")) << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
        << (direct ? " direct-lds" : " staged") << (ragged_groups ? " ragged-groups" : "")
        << (ops[0].edge || ops[1].edge || cedge ? " edges" : "") << " stages " << nstages << " lds " << nstages * stage_bytes

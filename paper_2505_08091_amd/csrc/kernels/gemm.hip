@@ -32,6 +32,9 @@
 //       operand (Section III-D partial tiles): load vector u is inside (1) or
 //       padding (0, read as zero); the operand's size in bytes
 //   C_EDGE, c_ok(tm, tn, lane, w, mi, ni, r): the C element exists
+//   A_VR A_VC A_BIDX (and B_*): a load vector that is an A_VR x A_VC block of
+//       the tile; A_BIDX[r * A_VC + c] is the vector element at block (r, c),
+//       and each block row is stored to LDS as one A_VC-element vector
 
 typedef unsigned short elem_t;
 typedef elem_t av_t __attribute__((ext_vector_type(A_V)));
@@ -179,7 +182,16 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
       if (A_GUARD && (IDX_T)u * NT + tid >= A_NVEC) continue;
-#if A_SVEC
+#if A_VR > 1 && A_SVEC
+      typedef elem_t ar_t __attribute__((ext_vector_type(A_VC)));
+#pragma unroll
+      for (int r = 0; r < A_VR; ++r) {
+        ar_t piece;
+#pragma unroll
+        for (int c = 0; c < A_VC; ++c) piece[c] = ra[rbuf][u][A_BIDX[r * A_VC + c]];
+        *(ar_t*)(la + a_s(tid, u, A_BIDX[r * A_VC])) = piece;
+      }
+#elif A_SVEC
       *(av_t*)(la + a_s(tid, u, 0)) = ra[rbuf][u];
 #else
 #pragma unroll
@@ -189,7 +201,16 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
       if (B_GUARD && (IDX_T)u * NT + tid >= B_NVEC) continue;
-#if B_SVEC
+#if B_VR > 1 && B_SVEC
+      typedef elem_t br_t __attribute__((ext_vector_type(B_VC)));
+#pragma unroll
+      for (int r = 0; r < B_VR; ++r) {
+        br_t piece;
+#pragma unroll
+        for (int c = 0; c < B_VC; ++c) piece[c] = rb[rbuf][u][B_BIDX[r * B_VC + c]];
+        *(br_t*)(lb + b_s(tid, u, B_BIDX[r * B_VC])) = piece;
+      }
+#elif B_SVEC
       *(bv_t*)(lb + b_s(tid, u, 0)) = rb[rbuf][u];
 #else
 #pragma unroll
@@ -256,7 +277,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       if (s == STORE_AT) {
         // Spread the LDS stores between the MFMAs of this substep.
 #pragma unroll
-        for (int g = 0; g < A_NV * (A_SVEC ? 1 : A_V) + B_NV * (B_SVEC ? 1 : B_V); ++g) {
+        for (int g = 0; g < A_NV * (A_SVEC ? A_VR : A_V) + B_NV * (B_SVEC ? B_VR : B_V); ++g) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
           __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // one LDS write
         }
@@ -413,7 +434,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
       if (s == STORE_AT) {
 #pragma unroll
-        for (int g = 0; g < A_NV * (A_SVEC ? 1 : A_V) + B_NV * (B_SVEC ? 1 : B_V); ++g) {
+        for (int g = 0; g < A_NV * (A_SVEC ? A_VR : A_V) + B_NV * (B_SVEC ? B_VR : B_V); ++g) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
         }
