@@ -254,7 +254,8 @@ def _gemm_ms(L, a_buf, b_buf, c_buf, n, dtype, reps, **kw):
 
 
 def bench_extra(L, reps=20):
-    """The other measured workloads: transposing remaps (Row <-> Col fp32,
+    """The other measured workloads: index maps of the blocked layout on the
+    device, the 128^3 and 1024^3 GEMMs, transposing remaps (Row <-> Col fp32,
     the 2D transpose of Section V-C), Row <-> Morton fp16 4096^2 hot and with
     the last-level cache flushed, the 4096^3 fp16 GEMM with A in Morton order
     and B row-major, the four Row/Col operand layouts of an 8192^3 fp16 GEMM
@@ -268,6 +269,46 @@ def bench_extra(L, reps=20):
         return round(nbytes / (ms * 1e-3) / 1e9, 1)
 
     out = {}
+    # Index maps on the device (out[x] = apply(x), out[p] = inv(p)) of the
+    # 8192^2 blocked layout, int32 outputs: pure write streams.
+    n = 8192
+    blk = L.TileOrderBy(L.Col(n // 64, n // 64), L.Row(64, 64))
+    o1 = torch.empty(n * n, dtype=torch.int32, device="cuda")
+    o2 = torch.empty(2 * n * n, dtype=torch.int32, device="cuda")
+    for _ in range(5):
+        L.apply_all_device(blk, o1)
+        L.inv_all_device(blk, o2)
+    ev = HipEvents(2 * reps + 1, _stream())
+    torch.cuda.synchronize()
+    for k in range(reps):
+        ev.record(2 * k)
+        L.apply_all_device(blk, o1)
+        ev.record(2 * k + 1)
+        L.inv_all_device(blk, o2)
+    ev.record(2 * reps)
+    torch.cuda.synchronize()
+    fa = sum(ev.ms(2 * k, 2 * k + 1) for k in range(reps)) / reps
+    fi = sum(ev.ms(2 * k + 1, 2 * k + 2) for k in range(reps)) / reps
+    ev.close()
+    out["index_maps_i32_8192_blocked"] = {"apply_bytes": 4 * n * n, "apply_GBps": gbps(4 * n * n, fa),
+                                          "inv_bytes": 8 * n * n, "inv_GBps": gbps(8 * n * n, fi),
+                                          "frac_hbm": round((12 * n * n) / ((fa + fi) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+    del o1, o2
+
+    # The smaller GEMM configurations: 128^3 fp16 with 64x64 tiles of 16x16
+    # wave tiles, and 1024^3 fp16 with 128x128x32 tiles, 64x64 wave tiles and
+    # a group of 8 (launch-bound: 64 workgroups on 256 CUs).
+    small = {}
+    for n, kw in ((128, dict(bm=64, bn=64, bk=32, wm=16, wn=16)),
+                  (1024, dict(bm=128, bn=128, bk=32, wm=64, wn=64, group_m=8))):
+        a = S.tensor(n * n, "f16", seed=S.SEED_A).cuda()
+        b = S.tensor(n * n, "f16", seed=S.SEED_B).cuda()
+        c = torch.empty(n * n, dtype=torch.float32, device="cuda")
+        ms = _gemm_ms(L, a, b, c, n, "f16", reps, **kw)
+        small[f"f16_{n}"] = {"us": round(ms * 1e3, 2), "tflops": round(2.0 * n ** 3 / (ms * 1e-3) / 1e12, 2),
+                             "plan": L.gemm_plan(n, n, n, "f16", **kw)}
+    out["gemm_small"] = small
+
     tr = []
     for n in (2048, 4096, 8192):
         x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()

@@ -65,13 +65,17 @@ KernelPlan plan_index_eval(const Layout& l, int which, int idx_bytes) {
   }
   std::ostringstream s;
   s << header() << "#define IDX_T " << (wide ? "i64" : "u32") << "\n#define OUT_T "
-    << (idx_bytes == 4 ? "int" : "long long") << "\n#define RANK " << l.dims().size() << "\n#define NPOINTS "
+    << (idx_bytes == 4 ? "int" : "long long") << "\n#define PPT " << 16 / idx_bytes << "\n#define RANK "
+    << l.dims().size() << "\n#define NPOINTS "
     << n << "ull\n#define " << (which == 0 ? "LEGO_HAVE_APPLY" : "LEGO_HAVE_INV") << " 1\n"
     << fns << "// ---- template ----\n" << tpl_index_eval;
   k.src = s.str();
   k.kernel = which == 0 ? "lego_apply_all" : "lego_inv_all";
   k.block = 256;
-  k.grid = std::max(1ll, std::min((n + 255) / 256, 256ll * 64));
+  // outputs per workgroup per round: 256 threads x one 16-byte vector
+  const long long per_block = 256ll * (16 / idx_bytes);
+  const long long nout = which == 0 ? n : n * (long long)l.dims().size();
+  k.grid = std::max(1ll, std::min((nout + per_block - 1) / per_block, 256ll * 64));
   k.info = std::string(which == 0 ? "apply" : "inv") + (wide ? " i64" : " u32") + info;
   return k;
 }
