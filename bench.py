@@ -80,6 +80,12 @@ class HipEvents:
         self.ev = []
 
 
+def _median(xs):
+    xs = sorted(xs)
+    m = len(xs) // 2
+    return xs[m] if len(xs) % 2 else 0.5 * (xs[m - 1] + xs[m])
+
+
 def _stream():
     import torch
     return torch.cuda.current_stream().cuda_stream
@@ -157,6 +163,8 @@ def bench_remap(L, steps, warmup):
         "sha1": _source_sha1(L, "remap", row, blk, param=4),
         "total_ms": total_ms,
         "launch_ms": (sum(fwd) + sum(inv)) / (2 * steps),
+        "launch_median_ms": _median(fwd + inv),
+        "launch_min_ms": min(fwd + inv),
         "fwd_ms": sum(fwd) / steps,
         "inv_ms": sum(inv) / steps,
         "copy_ms": copy_ms,
@@ -184,10 +192,11 @@ def bench_gemm(L, steps, warmup):
     ev.record(steps)
     torch.cuda.synchronize()
     ms = ev.ms(0, steps) / steps
+    each = [ev.ms(k, k + 1) for k in range(steps)]
     ev.close()
     flops = 2.0 * n ** 3
     tf = flops / (ms * 1e-3) / 1e12
-    return {"ms": ms, "tflops": tf, "plan": plan, "a": a, "b": b, "c": c,
+    return {"ms": ms, "median_ms": _median(each), "min_ms": min(each), "tflops": tf, "plan": plan, "a": a, "b": b, "c": c,
             "sha1": _source_sha1(L, "gemm", M=n, N=n, K=n, dtype="bf16")}
 
 
@@ -520,7 +529,9 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": profiled_traffic("remap_direct_8192x8192_f32_row_to_blocked", r["sha1"]),
                      "kernel": "lego_remap_direct", "bytes_per_launch": r["bytes_per_launch"],
-                     "avg_launch_ms": round(r["launch_ms"], 5)},
+                     "avg_launch_ms": round(r["launch_ms"], 5),
+                     "median_launch_ms": round(r["launch_median_ms"], 5),
+                     "min_launch_ms": round(r["launch_min_ms"], 5)},
     }
     if not args.no_gemm:
         g = bench_gemm(L, args.gemm_steps, 5)
@@ -533,7 +544,8 @@ def main():
                          "unit": "TFLOP/s", "frac": round(g["tflops"] / BF16_PEAK_TFLOPS, 4),
                          "traffic": profiled_traffic("gemm_8192_bf16", g["sha1"]),
                          "kernel": "lego_gemm", "flops_per_launch": 2 * N_GEMM ** 3,
-                         "avg_launch_ms": round(g["ms"], 5)},
+                         "avg_launch_ms": round(g["ms"], 5), "median_launch_ms": round(g["median_ms"], 5),
+                         "min_launch_ms": round(g["min_ms"], 5)},
         }
         if not args.no_cpu_baseline:
             out["gemm"]["cpu_baseline"] = cpu_baseline_gemm(g["a"], g["b"])
