@@ -269,7 +269,7 @@ def bench_extra(L, reps=20):
     the last-level cache flushed, the 4096^3 fp16 GEMM with A in Morton order
     and B row-major, the four Row/Col operand layouts of an 8192^3 fp16 GEMM
     (Section V-A), partial tiles: a padding/cropping remap and an 8000^3
-    GEMM (Section III-D), and user-defined GenPs from expression text: a
+    GEMM (Section III-D), 3-D bricks of a 512^3 grid, and user-defined GenPs from expression text: a
     wavefront tile order and an LDS swizzle (Section III-B)."""
     import torch
     import synth_inputs as S
@@ -395,6 +395,25 @@ def bench_extra(L, reps=20):
     out["gemm_ragged_bf16_8000"] = {"tflops": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
                                     "plan": L.gemm_plan(n, n, n, "bf16")}
     del a, b, c
+
+    # 3-D bricks (the stencil data layout of Section V): a 512^3 fp32 grid
+    # between row-major order and bricks of 8^3 or 4^3 elements stored
+    # contiguously, bricks in row-major order.
+    n = 512
+    x = S.tensor(n ** 3, "f32", seed=S.SEED_SRC).cuda()
+    y, z = torch.empty_like(x), torch.empty_like(x)
+    row = L.as_layout(L.Row(n, n, n))
+    br = []
+    for b in (8, 4):
+        bricks = L.TileOrderBy(L.Row(n // b, n // b, n // b), L.Row(b, b, b))
+        f, i = _alternate(L, row, bricks, x, y, z, reps)
+        nb = 2 * n ** 3 * 4
+        br.append({"brick": b, "bytes_per_launch": nb, "row_to_bricks_GBps": gbps(nb, f),
+                   "bricks_to_row_GBps": gbps(nb, i),
+                   "frac_hbm": round(2 * nb / ((f + i) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                   "plan": L.remap_plan(row, bricks, 4)["info"]})
+    out["bricks_f32_512cubed"] = br
+    del x, y, z
 
     # User-defined GenPs from expression text: an 8192^2 fp32 array whose 64x64
     # tiles are stored in antidiagonal (wavefront) order, and the 8192^3 bf16

@@ -62,6 +62,28 @@ def test_remap_transpose(lego, n, dtype):
     assert (bits(out) == bits(src).reshape(n, n).T.ravel()).all()
 
 
+@pytest.mark.parametrize("b", [8, 4])
+def test_remap_bricks_512cubed_sampled(lego, b):
+    """512^3 fp32 Row <-> bricks of b^3 (the configuration the bench times):
+    200k sampled destination elements against the oracle's inverse, then the
+    round trip back to row-major must be the identity."""
+    import torch
+    dev = need_gpu()
+    n = 512
+    src = S.tensor(n ** 3, "f32", seed=S.SEED_SRC)
+    row, br = lego.as_layout(lego.Row(n, n, n)), lego.TileOrderBy(lego.Row(n // b, n // b, n // b), lego.Row(b, b, b))
+    obr, orow = OL.TileOrderBy(OL.Row(n // b, n // b, n // b), OL.Row(b, b, b)), OL.as_layout(OL.Row(n, n, n))
+    say(f"remap bricks {b}^3 of 512^3 plan={lego.remap_plan(row, br, 4)['info']}")
+    out = _run(lego, row, br, src, dev)
+    p = np.random.default_rng(b).integers(0, n ** 3, 200000)
+    q = orow.apply(obr.inv(p))
+    sb = bits(src)
+    assert (bits(out)[p] == sb[q]).all()
+    say(f"remap bricks {b}^3 of 512^3 back plan={lego.remap_plan(br, row, 4)['info']}")
+    back = _run(lego, br, row, out, dev)
+    assert (bits(back) == sb).all()
+
+
 def _small_cases(L):
     return [
         ("antidiag chain 6x6 (gather)",
@@ -84,6 +106,12 @@ def _small_cases(L):
         ("3-level blocked 512^2", L.as_layout(L.Row(512, 512)),
          L.TileOrderBy(L.Col(4, 4), L.Row(4, 4), L.Row(32, 32)),
          OL.as_layout(OL.Row(512, 512)), OL.TileOrderBy(OL.Col(4, 4), OL.Row(4, 4), OL.Row(32, 32))),
+        # 3-D bricks (the stencil data layout of Section V): small ragged bricks and 8^3 bricks
+        ("3-D bricks 2x5x3 of 6x10x12", L.as_layout(L.Row(6, 10, 12)), L.TileOrderBy(L.Row(3, 2, 4), L.Row(2, 5, 3)),
+         OL.as_layout(OL.Row(6, 10, 12)), OL.TileOrderBy(OL.Row(3, 2, 4), OL.Row(2, 5, 3))),
+        ("3-D bricks 8^3 of 128^3", L.as_layout(L.Row(128, 128, 128)),
+         L.TileOrderBy(L.Row(16, 16, 16), L.Row(8, 8, 8)),
+         OL.as_layout(OL.Row(128, 128, 128)), OL.TileOrderBy(OL.Row(16, 16, 16), OL.Row(8, 8, 8))),
     ]
 
 
@@ -98,9 +126,11 @@ def _expand_cases(L):
             ([1000, 1000], [1024, 1024], L.TileOrderBy(L.Col(16, 16), L.Row(64, 64)),
              OL.TileOrderBy(OL.Col(16, 16), OL.Row(64, 64))),
             ([999, 1001], [1024, 1024], L.TileOrderBy(L.Col(16, 16), L.Row(64, 64)),
-             OL.TileOrderBy(OL.Col(16, 16), OL.Row(64, 64)))):
+             OL.TileOrderBy(OL.Col(16, 16), OL.Row(64, 64))),
+            ([100, 99, 101], [104, 104, 104], L.TileOrderBy(L.Row(13, 13, 13), L.Row(8, 8, 8)),
+             OL.TileOrderBy(OL.Row(13, 13, 13), OL.Row(8, 8, 8)))):
         ls, os_ = pad(n, ne, L.as_layout(L.Row(*ne)), OL.as_layout(OL.Row(*ne)))
-        out.append((f"pad {n[0]}x{n[1]} into tiles of {ne[0]}x{ne[1]}", ls, tl, os_, to))
+        out.append((f"pad {'x'.join(map(str, n))} into {'x'.join(map(str, ne))}", ls, tl, os_, to))
     return out
 
 

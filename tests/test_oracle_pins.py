@@ -396,6 +396,27 @@ def test_remap_blocked_matches_numpy_reshape():
     assert (out == blocks.ravel()).all()
 
 
+def test_remap_3d_bricks_match_numpy_reshape():
+    """TileOrderBy of two 3-D Row pieces stores a grid as bricks (the 3-D
+    subdomains of Section V's stencil layout), bricks in row-major order,
+    row-major inside each brick: a 6-D reshape/transpose of the row-major
+    array.  With ExpandBy, a grid the bricks do not divide is zero-padded."""
+    nb, b = (3, 2, 4), (2, 5, 3)
+    n = [x * y for x, y in zip(nb, b)]
+    src = np.arange(int(np.prod(n)), dtype=np.int64)
+    bricks = L.TileOrderBy(L.Row(*nb), L.Row(*b))
+    out = R.remap(L.as_layout(L.Row(*n)), bricks, src)
+    exp = src.reshape(nb[0], b[0], nb[1], b[1], nb[2], b[2]).transpose(0, 2, 4, 1, 3, 5)
+    assert (out == exp.ravel()).all()
+    assert (R.remap(bricks, L.as_layout(L.Row(*n)), out) == src).all()
+    m = [5, 9, 10]  # padded to n = [6, 10, 12]
+    data = np.arange(1, int(np.prod(m)) + 1, dtype=np.int64)
+    out = R.remap(L.ExpandBy(m, n, L.as_layout(L.Row(*n))), bricks, data)
+    padded = np.pad(data.reshape(m), [(0, x - y) for x, y in zip(n, m)])
+    exp = padded.reshape(nb[0], b[0], nb[1], b[1], nb[2], b[2]).transpose(0, 2, 4, 1, 3, 5)
+    assert (out == exp.ravel()).all()
+
+
 def test_remap_inverse_roundtrip_and_multiset():
     rng = np.random.default_rng(2)
     a = L.as_layout(L.Row(16, 16))
