@@ -246,7 +246,9 @@ def _flushed(L, la, lb, x, y, z, scratch, reps):
     return f, i
 
 
-def _gemm_ms(L, a_buf, b_buf, c_buf, n, dtype, reps, warmup=10, **kw):
+def _gemm_ms(L, a_buf, b_buf, c_buf, n, dtype, reps, warmup=30, **kw):
+    """Mean launch duration after ``warmup`` untimed launches (the shader
+    clock needs ~20 back-to-back large GEMMs to settle)."""
     import torch
     for _ in range(warmup):
         L.gemm(a_buf, b_buf, c_buf, n, n, n, dtype, **kw)
@@ -365,7 +367,7 @@ def bench_extra(L, reps=20):
     for la in ("Row", "Col"):
         for lb in ("Row", "Col"):
             kw = dict(a=L.as_layout(getattr(L, la)(n, n)), b=L.as_layout(getattr(L, lb)(n, n)))
-            ms = _gemm_ms(L, a, b, c, n, "f16", 10, **kw)
+            ms = _gemm_ms(L, a, b, c, n, "f16", 20, **kw)
             var[f"A {la} B {lb}"] = round(2.0 * n ** 3 / (ms * 1e-3) / 1e12, 1)
     out["gemm_operand_layouts_f16_8192_tflops"] = var
     del a, b, c
@@ -390,7 +392,7 @@ def bench_extra(L, reps=20):
     a = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_A).cuda()
     b = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_B).cuda()
     c = torch.empty(n * n, dtype=torch.float32, device="cuda")
-    ms = _gemm_ms(L, a, b, c, n, "bf16", 10)
+    ms = _gemm_ms(L, a, b, c, n, "bf16", 20)
     tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
     out["gemm_ragged_bf16_8000"] = {"tflops": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
                                     "plan": L.gemm_plan(n, n, n, "bf16")}
@@ -445,7 +447,7 @@ def bench_extra(L, reps=20):
     c = torch.empty(n * n, dtype=torch.float32, device="cuda")
     sw = L.as_layout(L.GenPExpr([256, 64], "i * 64 + (((j / 8) ^ ((i / 2) % 8)) * 8) + j % 8",
                                 ["x / 64", "(((x % 64) / 8) ^ ((x / 128) % 8)) * 8 + x % 8"]))
-    ms = _gemm_ms(L, a, b, c, n, "bf16", 10, lds_a=sw, lds_b=sw)
+    ms = _gemm_ms(L, a, b, c, n, "bf16", 20, lds_a=sw, lds_b=sw)
     tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
     out["gemm_expression_lds_bf16_8192"] = {"tflops": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
                                             "plan": L.gemm_plan(n, n, n, "bf16", lds_a=sw, lds_b=sw)}

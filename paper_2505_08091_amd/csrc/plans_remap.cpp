@@ -1,5 +1,6 @@
 // Planning of index-map evaluation and layout remap kernels.
 #include <algorithm>
+#include <numeric>
 #include <sstream>
 #include <stdexcept>
 
@@ -98,30 +99,48 @@ void split_digit(std::vector<Dg>& d, size_t k, i64 f) {
   d.insert(d.begin() + k + 1, hi);
 }
 
+// The factor of b to take into a tile that may grow by at most `room`: the
+// divisor f <= room of b with the most factors of two (so vector runs stay
+// powers of two), the largest such; 1 if none.
+i64 tile_factor(i64 b, i64 room) {
+  i64 best = 1;
+  auto twos = [](i64 x) {
+    int t = 0;
+    while (x % 2 == 0) x /= 2, ++t;
+    return t;
+  };
+  for (i64 f = 2; f <= std::min(b, room); ++f)
+    if (b % f == 0 && (twos(f) > twos(best) || (twos(f) == twos(best) && f > best))) best = f;
+  return best;
+}
+
 // Mark the lowest digits (by destination weight if by_dst, else by source
-// weight) until their product reaches `target`, splitting one digit if needed.
+// weight) while their product stays within `target`, splitting the first
+// digit that does not fit at a factor that does.  The product never exceeds
+// `target` (with extents that have no small factors it may stay below it).
 void take_lowest(std::vector<Dg>& d, i64 target, bool by_dst) {
-  i64 cum = 1;
   for (;;) {
     std::vector<size_t> order(d.size());
     for (size_t k = 0; k < d.size(); ++k) order[k] = k;
     std::sort(order.begin(), order.end(), [&](size_t x, size_t y) { return by_dst ? d[x].a < d[y].a : d[x].c < d[y].c; });
-    cum = 1;
+    i64 cum = 1;
     bool again = false;
     for (size_t k : order) {
       if (cum >= target) break;
+      if (d[k].tile) {  // taken already (by the other side's selection)
+        if (cum * d[k].b > target) break;
+        cum *= d[k].b;
+        continue;
+      }
       if (cum * d[k].b <= target) {
         d[k].tile = true;
         cum *= d[k].b;
         continue;
       }
-      i64 need = target / cum;
-      if (target % cum == 0 && need > 1 && d[k].b % need == 0) {
-        split_digit(d, k, need);
+      const i64 f = tile_factor(d[k].b, target / cum);
+      if (f > 1) {
+        split_digit(d, k, f);
         again = true;  // indices changed; re-run the selection
-      } else {
-        d[k].tile = true;
-        cum *= d[k].b;
       }
       break;
     }
@@ -392,6 +411,8 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   }
   std::sort(d.begin(), d.end(), [](const Dg& x, const Dg& y) { return x.a < y.a; });
   const i64 TILE = tile_size(d);
+  // the tile selection keeps a tile within 64 KiB of LDS; never emit more
+  if (TILE * elem_bytes > (64 << 10)) throw Unsupported("remap LDS tile exceeds 64 KiB");
   const i64 G = N / TILE;
   // Tile-local orders.
   std::vector<size_t> td, ts, gd;
@@ -514,8 +535,18 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
           return f;
         }}},
       &wide, &info);
-  int NT = (int)std::min<i64>(256, std::min<i64>(TILE / VL, TILE / VS));
-  if (NT < 1 || (TILE / VL) % NT || (TILE / VS) % NT) throw Unsupported("LDS tile does not divide into vectors");
+  // Threads per workgroup: the largest divisor of both vector counts up to
+  // 256 (whole passes over the tile on either side); at least one wave.
+  const i64 nvg = std::gcd(TILE / VL, TILE / VS);
+  int NT = 1;
+  for (int t = 256; t >= 1; --t)
+    if (nvg % t == 0) {
+      NT = t;
+      break;
+    }
+  if (NT < 64 && NT != nvg) throw Unsupported("LDS tile does not divide into vectors");
+  // each thread holds TILE / NT elements in registers between the two phases
+  if (TILE * elem_bytes / NT > 512) throw Unsupported("LDS tile too large for its thread count");
   s << header() << "#define ELEM_T " << et << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define TILE " << TILE
     << "\n#define NELEM " << N << "ull\n#define NTILES " << G << "ull\n#define NT " << NT << "\n#define VL " << VL << "\n#define VS " << VS << "\n#define LDSW_CONTIG "
     << (contig ? 1 : 0) << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_LDS 1\n"

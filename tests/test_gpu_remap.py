@@ -106,6 +106,16 @@ def _small_cases(L):
         ("3-level blocked 512^2", L.as_layout(L.Row(512, 512)),
          L.TileOrderBy(L.Col(4, 4), L.Row(4, 4), L.Row(32, 32)),
          OL.as_layout(OL.Row(512, 512)), OL.TileOrderBy(OL.Col(4, 4), OL.Row(4, 4), OL.Row(32, 32))),
+        # transposes whose extents are not powers of two (LDS tiles of odd sizes,
+        # workgroups that are not whole waves)
+        ("transpose 1000x1000", L.as_layout(L.Row(1000, 1000)), L.as_layout(L.Col(1000, 1000)),
+         OL.as_layout(OL.Row(1000, 1000)), OL.as_layout(OL.Col(1000, 1000))),
+        ("transpose 999x1001", L.as_layout(L.Row(999, 1001)), L.as_layout(L.Col(999, 1001)),
+         OL.as_layout(OL.Row(999, 1001)), OL.as_layout(OL.Col(999, 1001))),
+        ("transpose 200x1000", L.as_layout(L.Row(200, 1000)), L.as_layout(L.Col(200, 1000)),
+         OL.as_layout(OL.Row(200, 1000)), OL.as_layout(OL.Col(200, 1000))),
+        ("transpose 192x320", L.as_layout(L.Row(192, 320)), L.as_layout(L.Col(192, 320)),
+         OL.as_layout(OL.Row(192, 320)), OL.as_layout(OL.Col(192, 320))),
         # 3-D bricks (the stencil data layout of Section V): small ragged bricks and 8^3 bricks
         ("3-D bricks 2x5x3 of 6x10x12", L.as_layout(L.Row(6, 10, 12)), L.TileOrderBy(L.Row(3, 2, 4), L.Row(2, 5, 3)),
          OL.as_layout(OL.Row(6, 10, 12)), OL.TileOrderBy(OL.Row(3, 2, 4), OL.Row(2, 5, 3))),
