@@ -54,3 +54,25 @@ def int_tensor(n, seed=SEED_SRC, bits=32):
     tests of 4-byte elements (a random permutation of arange(n))."""
     g = torch.Generator().manual_seed(int(seed))
     return torch.randperm(int(n), generator=g).to(torch.int32 if bits == 32 else torch.int64)
+
+
+def _byte_hash(i, seed):
+    """High byte of a 32-bit multiplicative hash of (index, seed); every
+    intermediate stays below 2^63 so int64 arithmetic is exact."""
+    lo, hi = i & 0xFFFFFFFF, i >> 32
+    h = (lo * 0x5BD1E995 + hi * 0x1B873593 + int(seed) * 0x27D4EB2F) & 0xFFFFFFFF
+    h = ((h ^ (h >> 15)) * 0x2C1B3C6D) & 0xFFFFFFFF
+    return (h >> 24) & 255
+
+
+def byte_pattern(start, count, seed=SEED_SRC, device="cpu"):
+    """uint8 elements start .. start+count-1 of a pseudo-random byte array of
+    any length (buffers beyond 2^32 elements are filled slice by slice, on
+    the device that holds them)."""
+    i = torch.arange(int(start), int(start) + int(count), dtype=torch.int64, device=device)
+    return _byte_hash(i, seed).to(torch.uint8)
+
+
+def byte_pattern_at(idx, seed=SEED_SRC):
+    """The same bytes at the int64 numpy indices ``idx``."""
+    return _byte_hash(np.asarray(idx, dtype=np.int64), seed).astype(np.uint8)

@@ -39,6 +39,11 @@ def test_version_and_last_error(lego):
     (lambda L: L.RegP([2, 3], [1, 1]), "NOT_PERMUTATION"),
     (lambda L: L.RegP([2, 0], [1, 2]), "INVALID_ARG"),
     (lambda L: L.RegP([2, 3], [1]), "INVALID_ARG"),
+    # empty extents: every layout and GEMM dimension must be positive
+    (lambda L: L.Row(0, 4), "INVALID_ARG"),
+    (lambda L: L.GroupBy([4, 0]), "INVALID_ARG"),
+    (lambda L: L.gemm_plan(0, 64, 64, "f16"), "INVALID_ARG"),
+    (lambda L: L.gemm_plan(64, 64, 0, "bf16"), "INVALID_ARG"),
     (lambda L: L.GroupBy([4, 4]).OrderBy(L.Row(3, 5)), "SIZE_MISMATCH"),
     (lambda L: L.GenP("morton", [6, 8]), "INVALID_ARG"),
     (lambda L: L.GenP("xor_swizzle", [8, 24], [8, 1]), "INVALID_ARG"),

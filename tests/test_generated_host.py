@@ -115,6 +115,57 @@ int main(int argc, char** argv) {
 }
 """
 
+# Bounds and bijectivity of a remap too large to simulate element by element:
+# one bit per destination element written and per source element read.
+HARNESS_REMAP_BITS = r"""
+struct Bits {
+  std::vector<unsigned long long> w;
+  explicit Bits(u64 n) : w((n + 63) / 64) {}
+  bool set(u64 i) { unsigned long long m = 1ull << (i % 64), o = w[i / 64]; w[i / 64] = o | m; return o & m; }
+  bool all(u64 n) const { for (u64 i = 0; i < n; ++i) if (!(w[i / 64] >> (i % 64) & 1)) return false; return true; }
+};
+int main() {
+  // vectors are aligned runs, so one bit per source / destination vector
+#ifdef LEGO_REMAP_DIRECT
+  {  // the workgroup -> chunk schedule is a bijection onto the chunks
+    const u64 chunk = (u64)NT * UNROLL, nblk = (NVEC + chunk - 1) / chunk;
+    Bits hit(nblk);
+    for (u64 b = 0; b < nblk; ++b) {
+      u64 c = (u64)blk((IDX_T)b);
+      if (c >= nblk || hit.set(c)) FAIL("blk is not a bijection");
+    }
+  }
+  Bits rd(NSRC / V), wr(NVEC);
+  for (u64 t = 0; t < NVEC; ++t) {
+    u64 s = (u64)src_vec((IDX_T)t);
+    if ((s + 1) * V > NSRC) FAIL("src_vec out of range");
+    if (rd.set(s)) FAIL("source read twice");
+    wr.set(t);
+  }
+  if (!rd.all(NSRC / V) || !wr.all(NVEC)) FAIL("element never copied");
+#else
+  const u64 n = NELEM;
+  if (NT < 1 || NT > 256 || (TILE / VL) % NT || (TILE / VS) % NT) FAIL("NT does not divide the tile's vectors");
+  Bits rd(n / VL), wr(n / VS);
+  for (u64 g = 0; g < NTILES; ++g) {
+    for (u64 q = 0; q < TILE / VL; ++q) {
+      u64 s = (u64)src_off((IDX_T)g, (IDX_T)q);
+      if (s % VL || s + VL > n) FAIL("src_off out of range");
+      if (rd.set(s / VL)) FAIL("source read twice");
+    }
+    for (u64 q = 0; q < TILE / VS; ++q) {
+      u64 d = (u64)dst_off((IDX_T)g, (IDX_T)q);
+      if (d % VS || d + VS > n) FAIL("dst_off out of range");
+      if (wr.set(d / VS)) FAIL("destination written twice");
+    }
+  }
+  if (!rd.all(n / VL) || !wr.all(n / VS)) FAIL("element never copied");
+#endif
+  printf("ok\n");
+  return 0;
+}
+"""
+
 HARNESS_GEMM = r"""
 static u64 goff_a(u64 tm, u64 kt, u64 tid, u64 u) {
 #if A_SEP
@@ -370,6 +421,26 @@ def test_remap_sources_of_gpu_cases(elem_bytes):
                 # source element k is tagged k + 1, so zero fill reads as -1
                 exp = OR.remap(oa, ob, np.arange(1, OR.phys_size(oa) + 1, dtype=np.int64)) - 1
                 assert (perm == exp).all(), (name, elem_bytes)
+
+
+def _huge_remap_cases():
+    """Remaps of 65600^2 one-byte elements (more than 2^32, so byte and element
+    offsets need 64 bits; 65600 = 64 * 1025 has odd factors)."""
+    import paper_2505_08091_amd as L
+    n = 65600
+    row = L.as_layout(L.Row(n, n))
+    return [("row -> 64x64 blocked", row, L.TileOrderBy(L.Col(n // 64, n // 64), L.Row(64, 64))),
+            ("row -> col", row, L.as_layout(L.Col(n, n)))]
+
+
+@pytest.mark.slow
+def test_remap_sources_beyond_4g_elements():
+    import paper_2505_08091_amd as L
+    with tempfile.TemporaryDirectory() as tmp:
+        for name, ls, ld in _huge_remap_cases():
+            for a, b in ((ls, ld), (ld, ls)):
+                src = L.plan_source("remap", a, b, param=1)
+                assert _compile_and_run(src, HARNESS_REMAP_BITS, tmp).strip() == "ok", name
 
 
 def _gemm_cases():

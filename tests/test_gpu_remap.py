@@ -84,6 +84,41 @@ def test_remap_bricks_512cubed_sampled(lego, b):
     assert (bits(back) == sb).all()
 
 
+def test_remap_beyond_4g_elements(lego):
+    """65600^2 one-byte elements (more than 2^32; 65600 = 64 * 1025): Row to
+    64x64 blocked (direct path) and Row to Col (LDS path, 64-bit offsets).
+    The first and last 4096 and 10^6 random destination elements against the
+    oracle, then the round trip back must be the identity."""
+    import torch
+    dev = need_gpu()
+    n = 65600
+    N = n * n
+    src = torch.empty(N, dtype=torch.uint8, device=dev)
+    for s0 in range(0, N, 1 << 28):
+        c = min(1 << 28, N - s0)
+        src[s0:s0 + c] = S.byte_pattern(s0, c, device=dev)
+    rng = np.random.default_rng(5)
+    p = np.concatenate([np.arange(4096), N - 4096 + np.arange(4096), rng.integers(0, N, 1_000_000)])
+    pt = torch.from_numpy(p).to(dev)
+    row, orow = lego.as_layout(lego.Row(n, n)), OL.as_layout(OL.Row(n, n))
+    for name, ld, old in (
+            ("blocked", lego.TileOrderBy(lego.Col(n // 64, n // 64), lego.Row(64, 64)),
+             OL.TileOrderBy(OL.Col(n // 64, n // 64), OL.Row(64, 64))),
+            ("col", lego.as_layout(lego.Col(n, n)), OL.as_layout(OL.Col(n, n)))):
+        say(f"remap 65600^2 u8 row->{name} plan={lego.remap_plan(row, ld, 1)['info']}")
+        dst = torch.empty_like(src)
+        lego.remap(row, ld, src, dst)
+        torch.cuda.synchronize()
+        exp = S.byte_pattern_at(orow.apply(old.inv(p)))
+        assert (dst[pt].cpu().numpy() == exp).all(), name
+        say(f"remap 65600^2 u8 {name}->row plan={lego.remap_plan(ld, row, 1)['info']}")
+        back = torch.empty_like(src)
+        lego.remap(ld, row, dst, back)
+        torch.cuda.synchronize()
+        assert torch.equal(back, src), name
+        del dst, back
+
+
 def _small_cases(L):
     return [
         ("antidiag chain 6x6 (gather)",

@@ -600,3 +600,14 @@ def test_expression_morton_and_row_col():
     s = GX.expr_genp([256, 64], GE.SWIZZLE64_APPLY, GE.SWIZZLE64_INV)
     i, j = np.meshgrid(np.arange(256), np.arange(64), indexing="ij")
     assert (s.apply([i, j]) == L.xor_swizzle_genp(256, 64, 8, 2).apply([i, j])).all()
+
+
+def test_byte_pattern_slices_agree():
+    """The large-buffer byte generator: any slice equals the values at those
+    indices, beyond 2^32 too, and the bytes are spread over 0..255."""
+    import synth_inputs as S
+    for start in (0, (1 << 32) - 100, 5 << 32):
+        a = S.byte_pattern(start, 1000).numpy()
+        assert (a == S.byte_pattern_at(np.arange(start, start + 1000))).all()
+    v = S.byte_pattern(0, 1 << 16).numpy()
+    assert len(np.unique(v)) == 256 and abs(v.mean() - 127.5) < 3
