@@ -239,7 +239,15 @@ lego_status lego_mfma_fragment_layout(int instr, int operand, lego_layout_t* out
 
 /* Compile every generated kernel source for the built-in test and benchmark
  * configurations with hipRTC (no GPU needed).  Returns the number of sources
- * compiled in *count.  Used by the build check. */
+ * compiled in *count; info (may be NULL) gets a first line naming the
+ * compiler ("compiler: hipRTC <major>.<minor> from <library>"), then one
+ * line per source with its compile time.  Used by the build check.
+ *
+ * Kernels are compiled by the hipRTC of the installed ROCm (ROCM_PATH,
+ * default /opt/rocm), loaded into a link namespace of its own so that a
+ * host process carrying another ROCm release's compiler library does not
+ * substitute it.  LEGO_DUMP=<dir> keeps each generated source and its code
+ * object there. */
 lego_status lego_selftest_compile(int* count, char* info, size_t info_cap);
 
 /* The generated kernel source a device call would compile (for inspection and

@@ -527,6 +527,7 @@ lego_status lego_selftest_compile(int* count, char* info, size_t info_cap) {
   return guard([&] {
     std::vector<std::pair<std::string, std::string>> srcs = selftest_sources();
     std::ostringstream s;
+    s << "compiler: " << jit_compiler() << "\n";
     int n = 0;
     for (auto& [name, src] : srcs) {
       std::string log;

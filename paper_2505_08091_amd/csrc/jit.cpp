@@ -1,6 +1,7 @@
 // hipRTC compilation and code-object caching.  See jit.hpp.
 #include "jit.hpp"
 
+#include <dlfcn.h>
 #include <hip/hiprtc.h>
 #include <sys/stat.h>
 #include <unistd.h>
@@ -22,6 +23,66 @@ std::mutex g_mu;
 std::map<std::string, JitKernel> g_mem;         // key + device + name -> function
 std::map<std::string, hipModule_t> g_modules;   // key + device -> module
 JitStats g_stats;
+
+// hipRTC of the installed ROCm (ROCM_PATH, default /opt/rocm), loaded into a
+// link namespace of its own.  hipRTC opens its compiler library (comgr) by
+// soname at run time; a host process that already carries another ROCm
+// release's comgr (a PyTorch wheel bundles one) would otherwise hand it that
+// older compiler, whose code for the one-wave-per-SIMD GEMM spills its
+// accumulators to scratch.  The namespace keeps the installed compiler.  If
+// the private load fails, the hipRTC the process resolves normally is used.
+struct Rtc {
+  hiprtcResult (*version)(int*, int*);
+  hiprtcResult (*create)(hiprtcProgram*, const char*, const char*, int, const char**, const char**);
+  hiprtcResult (*compile)(hiprtcProgram, int, const char**);
+  hiprtcResult (*log_size)(hiprtcProgram, size_t*);
+  hiprtcResult (*log)(hiprtcProgram, char*);
+  hiprtcResult (*code_size)(hiprtcProgram, size_t*);
+  hiprtcResult (*code)(hiprtcProgram, char*);
+  hiprtcResult (*destroy)(hiprtcProgram*);
+  std::string origin;
+};
+
+const Rtc& rtc() {
+  static const Rtc r = [] {
+    const char* root = std::getenv("ROCM_PATH");
+    std::string path = std::string(root && *root ? root : "/opt/rocm") + "/lib/libhiprtc.so.7";
+    void* h = dlmopen(LM_ID_NEWLM, path.c_str(), RTLD_NOW | RTLD_LOCAL);
+    std::string origin = path + " (private namespace)";
+    if (!h) {
+      h = dlopen("libhiprtc.so.7", RTLD_NOW | RTLD_LOCAL);
+      origin = "libhiprtc.so.7 (process namespace)";
+    }
+    if (!h) throw std::runtime_error("hipRTC library not found");
+    auto sym = [&](const char* name) {
+      void* f = dlsym(h, name);
+      if (!f) throw std::runtime_error(std::string("hipRTC symbol missing: ") + name);
+      return f;
+    };
+    Rtc t;
+    t.version = (decltype(t.version))sym("hiprtcVersion");
+    t.create = (decltype(t.create))sym("hiprtcCreateProgram");
+    t.compile = (decltype(t.compile))sym("hiprtcCompileProgram");
+    t.log_size = (decltype(t.log_size))sym("hiprtcGetProgramLogSize");
+    t.log = (decltype(t.log))sym("hiprtcGetProgramLog");
+    t.code_size = (decltype(t.code_size))sym("hiprtcGetCodeSize");
+    t.code = (decltype(t.code))sym("hiprtcGetCode");
+    t.destroy = (decltype(t.destroy))sym("hiprtcDestroyProgram");
+    t.origin = origin;
+    return t;
+  }();
+  return r;
+}
+
+}  // namespace
+
+std::string jit_compiler() {
+  int major = 0, minor = 0;
+  rtc().version(&major, &minor);
+  return "hipRTC " + std::to_string(major) + "." + std::to_string(minor) + " from " + rtc().origin;
+}
+
+namespace {
 
 uint64_t fnv1a(const std::string& s, uint64_t h = 1469598103934665603ull) {
   for (unsigned char ch : s) {
@@ -59,7 +120,7 @@ void mkdirs(const std::string& path) {
 
 std::string source_key(const std::string& src) {
   int major = 0, minor = 0;
-  hiprtcVersion(&major, &minor);
+  rtc().version(&major, &minor);
   std::string k = src;
   for (auto& o : jit_options()) k += "\x1f" + o;
   k += "\x1fhiprtc" + std::to_string(major) + "." + std::to_string(minor);
@@ -128,26 +189,34 @@ std::vector<char> jit_compile(const std::string& src, std::string* log, double* 
       f << src;
     }
   }
+  const Rtc& R = rtc();
   hiprtcProgram prog;
-  if (hiprtcCreateProgram(&prog, src.c_str(), "lego_generated.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS)
+  if (R.create(&prog, src.c_str(), "lego_generated.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS)
     throw std::runtime_error("hiprtcCreateProgram failed");
   std::vector<const char*> o;
   for (auto& s : jit_options()) o.push_back(s.c_str());
-  hiprtcResult rc = hiprtcCompileProgram(prog, (int)o.size(), o.data());
+  hiprtcResult rc = R.compile(prog, (int)o.size(), o.data());
   size_t n = 0;
-  hiprtcGetProgramLogSize(prog, &n);
+  R.log_size(prog, &n);
   std::string lg(n, '\0');
-  if (n) hiprtcGetProgramLog(prog, &lg[0]);
+  if (n) R.log(prog, &lg[0]);
   if (log) *log = lg;
   if (rc != HIPRTC_SUCCESS) {
-    hiprtcDestroyProgram(&prog);
+    R.destroy(&prog);
     throw std::runtime_error("hipRTC compilation failed:\n" + lg);
   }
   size_t cs = 0;
-  hiprtcGetCodeSize(prog, &cs);
+  R.code_size(prog, &cs);
   std::vector<char> code(cs);
-  hiprtcGetCode(prog, code.data());
-  hiprtcDestroyProgram(&prog);
+  R.code(prog, code.data());
+  R.destroy(&prog);
+  if (const char* dump = std::getenv("LEGO_DUMP")) {
+    if (*dump) {
+      mkdirs(dump);
+      std::ofstream f(std::string(dump) + "/" + source_key(src) + ".co", std::ios::binary);
+      f.write(code.data(), (std::streamsize)code.size());
+    }
+  }
   auto t1 = std::chrono::steady_clock::now();
   if (ms) *ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
   return code;

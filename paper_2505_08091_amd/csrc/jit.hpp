@@ -31,6 +31,10 @@ std::vector<char> jit_compile(const std::string& src, std::string* log, double* 
 // Options passed to hipRTC (also recorded in the cache key).
 const std::vector<std::string>& jit_options();
 
+// "hipRTC <major>.<minor> from <library> (<namespace>)": the compiler behind
+// jit_compile.
+std::string jit_compiler();
+
 struct JitStats {
   long compiles = 0, disk_hits = 0, mem_hits = 0;
   double compile_ms = 0;

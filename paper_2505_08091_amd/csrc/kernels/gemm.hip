@@ -136,17 +136,25 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // the tile for step kt+2 is loaded while the tile for step kt+1 (loaded one
   // step earlier) is written to LDS, hiding more than a full step of memory
   // latency.
-  av_t ra[PREFETCH][A_NV];
-  bv_t rb[PREFETCH][B_NV];
+#if PREFETCH == 2 && BK / KB >= 2
+#define NSETS 1  // the rolling pipeline below reuses one set
+#else
+#define NSETS PREFETCH
+#endif
+  av_t ra[NSETS][A_NV];
+  bv_t rb[NSETS][B_NV];
   acc_t acc[MI][NI];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = (acc_t){};
 
-  auto gload = [&](IDX_T kt, int rbuf) {
+  // Load vectors [lo, hi) of the tile for step kt (A's A_NV vectors, then
+  // B's B_NV) into staging set rbuf.
+  auto gload_part = [&](IDX_T kt, int rbuf, int lo, int hi) {
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
+      if (u < lo || u >= hi) continue;
       if (A_GUARD && (IDX_T)u * NT + tid >= A_NVEC) continue;
 #if A_EDGE
       if (!a_ok(tm, kt, tid, u)) {
@@ -162,6 +170,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     }
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
+      if (A_NV + u < lo || A_NV + u >= hi) continue;
       if (B_GUARD && (IDX_T)u * NT + tid >= B_NVEC) continue;
 #if B_EDGE
       if (!b_ok(tn, kt, tid, u)) {
@@ -176,11 +185,14 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #endif
     }
   };
-  auto sstore = [&](int stage, int rbuf) {
+  auto gload = [&](IDX_T kt, int rbuf) { gload_part(kt, rbuf, 0, A_NV + B_NV); };
+  // Write vectors [lo, hi) of staging set rbuf to LDS stage `stage`.
+  auto sstore_part = [&](int stage, int rbuf, int lo, int hi) {
     elem_t* la = lds + stage * STAGE;
     elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
+      if (u < lo || u >= hi) continue;
       if (A_GUARD && (IDX_T)u * NT + tid >= A_NVEC) continue;
 #if A_VR > 1 && A_SVEC
       typedef elem_t ar_t __attribute__((ext_vector_type(A_VC)));
@@ -200,6 +212,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     }
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
+      if (A_NV + u < lo || A_NV + u >= hi) continue;
       if (B_GUARD && (IDX_T)u * NT + tid >= B_NVEC) continue;
 #if B_VR > 1 && B_SVEC
       typedef elem_t br_t __attribute__((ext_vector_type(B_VC)));
@@ -218,6 +231,8 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #endif
     }
   };
+
+  auto sstore = [&](int stage, int rbuf) { sstore_part(stage, rbuf, 0, A_NV + B_NV); };
 
   // Fragments of one k-substep, double-buffered in registers: the reads of
   // substep s+1 are in flight while the MFMAs of substep s run.
@@ -400,6 +415,63 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+#elif PREFETCH == 2 && BK / KB >= 2
+  // One wave per SIMD (the accumulators fill the AGPRs): no other wave hides
+  // a stall, so each step overlaps all of its memory traffic with its MFMAs.
+  // One staging set rolls through the tiles: during step t-1, in the
+  // substeps before the last, each part of tile t is written from the set
+  // to LDS stage t&1, and one substep later the same part of tile t+1 is
+  // loaded into the freed registers (about a step ahead of its own LDS
+  // write).  A barrier ahead of
+  // the last substep publishes tile t, and that substep's MFMAs run under
+  // the first fragment reads of step t.  Stage t&1 was last read in step
+  // t-2, before that step's barrier.
+  constexpr int S = BK / KB;
+  constexpr int NL = A_NV + B_NV;  // load / store vectors per thread and tile
+  auto pipe_step = [&](IDX_T kt) {
+    const int cur = kt & 1;
+    const elem_t* la = lds + cur * STAGE;
+    const elem_t* lb = la + A_STAGE;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      FRAG_WAIT();
+      if (s == S - 1) {
+        // this wave's stores of tile kt+1 are issued; once every wave's
+        // have landed, stage (kt+1)&1 may be read
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      if (s + 1 < S) fload(la, lb, s + 1, (s + 1) & 1);
+      else if (kt + 1 < KT) {
+        const elem_t* na = lds + (cur ^ 1) * STAGE;
+        fload(na, na + A_STAGE, 0, 0);
+      }
+      // Part s of tile kt+1 goes to LDS; part s-1, written one substep
+      // earlier, is reloaded with tile kt+2 (reloading registers that an LDS
+      // write still has to read would stall the wave until that write drains).
+      if (s < S - 1 && kt + 1 < KT) sstore_part(cur ^ 1, 0, s * NL / (S - 1), (s + 1) * NL / (S - 1));
+      if (s > 0 && kt + 2 < KT) gload_part(kt + 2, 0, (s - 1) * NL / (S - 1), s * NL / (S - 1));
+      // one MFMA, then one of each kind of memory instruction, while they last
+#pragma unroll
+      for (int g = 0; g < MI * NI; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  gload(0, 0);
+  sstore(0, 0);
+  if (1 < KT) gload(1, 0);
+  __syncthreads();
+  fload(lds, lds + A_STAGE, 0, 0);
+  for (IDX_T kt = 0; kt < KT; ++kt) pipe_step(kt);
 #elif PREFETCH == 2
   gload(0, 0);
   if (1 < KT) gload(1, 1);

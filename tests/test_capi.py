@@ -235,3 +235,28 @@ def test_expression_language_host(lego, text, value):
     a shift of a 1009-point tile by the expression's value exposes it."""
     g = lego.as_layout(lego.GenPExpr([1009], f"i + ({text})", [f"x - ({text})"]))
     assert g.apply([0]) == value % 1009
+
+
+def test_jit_uses_installed_compiler(tmp_path):
+    """Kernels are compiled by the installed ROCm's compiler even in a process
+    that imported a PyTorch wheel (which bundles an older compiler library
+    under the same soname) first: the code objects name the compiler that
+    /opt/rocm/llvm/bin/clang reports."""
+    import subprocess
+    import sys
+    clang = "/opt/rocm/llvm/bin/clang"
+    readelf = "/opt/rocm/llvm/bin/llvm-readelf"
+    if not (os.path.exists(clang) and os.path.exists(readelf)):
+        pytest.skip("no ROCm LLVM tools")
+    want = subprocess.run([clang, "--version"], capture_output=True, text=True).stdout.splitlines()[0].strip()
+    code = ("import torch\nimport paper_2505_08091_amd as L\n"
+            "print(L.selftest_compile()[1].splitlines()[0])\n")
+    env = dict(os.environ, LEGO_DUMP=str(tmp_path), PYTHONPATH=ROOT)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=600)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert "private namespace" in r.stdout, r.stdout
+    objs = sorted(tmp_path.glob("*.co"))
+    assert objs
+    for o in objs[:3]:
+        comment = subprocess.run([readelf, "-p", ".comment", str(o)], capture_output=True, text=True).stdout
+        assert want in comment, (want, comment)
