@@ -45,6 +45,26 @@ LEGO_FN void remap_chunk(const vec_t* __restrict__ src, vec_t* __restrict__ dst,
 #define SRC_OF(t, u) (src + src_vec((IDX_T)(t)))
 #endif
   vec_t v[UNROLL];
+  if ((c + 1) * (NT * UNROLL) <= NVEC) {
+    // A whole chunk (every chunk but a ragged last one): no bounds tests, so
+    // the UNROLL loads are issued back to back.  A vector without a source
+    // reads the buffer's first vector instead and is zeroed, keeping the
+    // loads free of branches.
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const u64 t = base + (u64)u * NT;
+#if MASKED
+      const bool ok = src_ok((IDX_T)t);
+      const vec_t x = LEGO_LD(ok ? SRC_OF(t, u) : src);
+      v[u] = ok ? x : (vec_t){};
+#else
+      v[u] = LEGO_LD(SRC_OF(t, u));
+#endif
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) LEGO_ST(v[u], dst + base + (u64)u * NT);
+    return;
+  }
 #pragma unroll
   for (int u = 0; u < UNROLL; ++u) {
     const u64 t = base + (u64)u * NT;
