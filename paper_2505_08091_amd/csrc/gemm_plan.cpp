@@ -723,8 +723,14 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   int prefetch = (MI * NI * NREG > 128) ? 2 : 1;
   if (const char* e = std::getenv("LEGO_GEMM_PREFETCH")) prefetch = std::atoi(e) == 2 ? 2 : 1;
   if (Kt < 2) prefetch = 1;
-  s << "#define PREFETCH " << prefetch << "\n#define DIRECT_LDS " << (direct ? 1 : 0) << "\n#define NSTAGES "
-    << nstages << "\n";
+  // Register-staged plans use the rolling pipeline (one staging set; LDS
+  // writes and reloads spread over the substeps): measured +7% on the 8192^3
+  // bf16 GEMM and +16% on the 4096^3 Morton-A GEMM over staging the whole
+  // tile in one substep.
+  int rolling = 1;
+  if (const char* e = std::getenv("LEGO_GEMM_ROLLING")) rolling = std::atoi(e) != 0;
+  s << "#define PREFETCH " << prefetch << "\n#define ROLLING " << rolling << "\n#define DIRECT_LDS " << (direct ? 1 : 0)
+    << "\n#define NSTAGES " << nstages << "\n";
   const char* store_env = std::getenv("LEGO_GEMM_STORE_AT");
   int store_at = store_env ? std::atoi(store_env) : (bk / KB) / 2;
   store_at = std::max(0, std::min(store_at, bk / KB - 1));

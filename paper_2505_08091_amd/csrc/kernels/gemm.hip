@@ -18,6 +18,7 @@
 //   C_SEP
 //   STORE_AT         k-substep during which the next tile is written to LDS
 //   PREFETCH         1 or 2: K steps between a tile's global load and its use
+//   ROLLING          1: register-staged loads use the rolling pipeline
 //   DIRECT_LDS       1: global-to-LDS copies without registers, NSTAGES-deep ring
 //   NSTAGES          LDS stages (2 unless DIRECT_LDS)
 //   sched(pid, &tm, &tn)
@@ -136,7 +137,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // the tile for step kt+2 is loaded while the tile for step kt+1 (loaded one
   // step earlier) is written to LDS, hiding more than a full step of memory
   // latency.
-#if PREFETCH == 2 && BK / KB >= 2
+#if (PREFETCH == 2 || ROLLING) && BK / KB >= 2
 #define NSETS 1  // the rolling pipeline below reuses one set
 #else
 #define NSETS PREFETCH
@@ -415,10 +416,11 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-#elif PREFETCH == 2 && BK / KB >= 2
-  // One wave per SIMD (the accumulators fill the AGPRs): no other wave hides
-  // a stall, so each step overlaps all of its memory traffic with its MFMAs.
-  // One staging set rolls through the tiles: during step t-1, in the
+#elif (PREFETCH == 2 || ROLLING) && BK / KB >= 2
+  // Register-staged pipeline.  With one wave per SIMD (the accumulators
+  // fill the AGPRs) no other wave hides a stall, and with two the loads and
+  // stores still cost less spread out: each step overlaps all of its memory
+  // traffic with its MFMAs.  One staging set rolls through the tiles: during step t-1, in the
   // substeps before the last, each part of tile t is written from the set
   // to LDS stage t&1, and one substep later the same part of tile t+1 is
   // loaded into the freed registers (about a step ahead of its own LDS

@@ -190,22 +190,30 @@ def _ragged_cases(L):
         dict(M=1000, N=1000, K=1000, dtype="f16", a=L.as_layout(L.Col(1000, 1000)), b=L.as_layout(L.Row(1000, 1000))),
         dict(M=77, N=1, K=5, dtype="f16"),
         dict(M=1, N=1, K=1, dtype="bf16"),
+        # register-staged loads (the rolling pipeline) with partial tiles: A in
+        # 2x4 blocks (4-element k runs), then also B in 4x8 column-major blocks
+        # (element loads)
+        dict(M=1002, N=520, K=1000, dtype="bf16", a=L.TileOrderBy(L.Row(501, 250), L.Row(2, 4)),
+             oa=OL.TileOrderBy(OL.Row(501, 250), OL.Row(2, 4))),
+        dict(M=1002, N=520, K=1000, dtype="f16", a=L.TileOrderBy(L.Row(501, 250), L.Row(2, 4)),
+             b=L.TileOrderBy(L.Row(250, 65), L.Col(4, 8)),
+             oa=OL.TileOrderBy(OL.Row(501, 250), OL.Row(2, 4)), ob=OL.TileOrderBy(OL.Row(250, 65), OL.Col(4, 8))),
     ]
 
 
-@pytest.mark.parametrize("i", range(8))
+@pytest.mark.parametrize("i", range(10))
 def test_gemm_ragged_sizes(lego, i):
     """Every output element of a GEMM with partial tiles against the oracle;
     C is pre-filled with NaN so a dropped or misplaced store shows."""
     kw = dict(_ragged_cases(lego)[i])
     M, N, K, dtype = kw.pop("M"), kw.pop("N"), kw.pop("K"), kw.pop("dtype")
+    oa, ob = kw.pop("oa", None), kw.pop("ob", None)
     a = S.tensor(M * K, dtype, seed=S.SEED_A)
     b = S.tensor(K * N, dtype, seed=S.SEED_B)
     say(f"gemm ragged {M}x{N}x{K} {dtype} plan={lego.gemm_plan(M, N, K, dtype, **kw)}")
     c = _run(lego, a, b, M, N, K, dtype, **kw).reshape(M, N)
-    la = kw["a"] if "a" in kw else None
-    ola = OL.as_layout(OL.Col(M, K)) if la is not None else OL.as_layout(OL.Row(M, K))
-    olb = OL.as_layout(OL.Row(K, N)) if "b" in kw else OL.as_layout(OL.Col(K, N))
+    ola = oa if oa is not None else OL.as_layout(OL.Col(M, K)) if "a" in kw else OL.as_layout(OL.Row(M, K))
+    olb = ob if ob is not None else OL.as_layout(OL.Row(K, N)) if "b" in kw else OL.as_layout(OL.Col(K, N))
     r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), ola, olb, dtype)
     assert np.isfinite(c).all()
     ok, mre, fre = OG.check_tolerance(c, r)
