@@ -387,11 +387,13 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   std::vector<Dg> d;
   for (auto& x : digits) d.push_back({x.a, x.b, x.coeff});
   // A remap whose traffic exceeds the 256 MB last-level cache streams from HBM:
-  // there 32 KiB tiles taken in source order measured fastest (8192^2 fp32
-  // transpose: +10-20% over 16 KiB tiles in destination order); smaller remaps
-  // keep 16 KiB tiles in destination order.
+  // there tiles taken in source order measured fastest, 32 KiB in general
+  // (3-D bricks, Morton) and 64 KiB when the map keeps no two neighbours
+  // together (run 1, a transpose: 512-byte runs on both sides of a 128x128
+  // fp32 tile, +9-13% over 32 KiB on the 8192^2 fp32 transpose); smaller
+  // remaps keep 16 KiB tiles in destination order.
   const bool hbm_bound = 2 * N * elem_bytes > (256ll << 20);
-  i64 tile_bytes = hbm_bound ? 32 * 1024 : 16 * 1024;
+  i64 tile_bytes = hbm_bound ? (run == 1 ? 64 * 1024 : 32 * 1024) : 16 * 1024;
   if (const char* e = std::getenv("LEGO_REMAP_TILE_BYTES")) tile_bytes = std::max<i64>(256, std::atoll(e));
   const i64 max_tile = std::min<i64>(N, std::max<i64>(32 * 1024, tile_bytes) / elem_bytes);
   i64 tdst = std::min<i64>(N, std::max<i64>(maxv, 256 / elem_bytes));
@@ -411,8 +413,8 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   }
   std::sort(d.begin(), d.end(), [](const Dg& x, const Dg& y) { return x.a < y.a; });
   const i64 TILE = tile_size(d);
-  // the tile selection keeps a tile within 64 KiB of LDS; never emit more
-  if (TILE * elem_bytes > (64 << 10)) throw Unsupported("remap LDS tile exceeds 64 KiB");
+  // never emit a tile beyond 128 KiB of LDS (160 KiB per CU)
+  if (TILE * elem_bytes > (128 << 10)) throw Unsupported("remap LDS tile exceeds 128 KiB");
   const i64 G = N / TILE;
   // Tile-local orders.
   std::vector<size_t> td, ts, gd;

@@ -73,7 +73,7 @@ int main(int argc, char** argv) {
 #else
   const u64 n = NELEM, nsrc = NELEM;
   if (NT < 1 || NT > 256 || (TILE / VL) % NT || (TILE / VS) % NT) FAIL("NT does not divide the tile's vectors");
-  if ((unsigned long long)TILE * sizeof(ELEM_T) > 65536) FAIL("LDS tile exceeds 64 KiB");
+  if ((unsigned long long)TILE * sizeof(ELEM_T) > 131072) FAIL("LDS tile exceeds 128 KiB");
   if ((unsigned long long)TILE * sizeof(ELEM_T) / NT > 512) FAIL("too many tile elements per thread");
   std::vector<long long> perm(n, -2);
   std::vector<long long> tile(TILE);
