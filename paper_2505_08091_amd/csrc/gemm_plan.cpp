@@ -150,7 +150,8 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   // of Section III-D): loads outside [M, K] / [K, N] read zero, stores outside
   // [M, N] are dropped.
   const bool edge_m = M % bm != 0, edge_n = N % bn != 0, edge_k = K % bk != 0;
-  const int MB = (wm % 32 == 0 && wn % 32 == 0) ? 32 : 16;
+  int MB = (wm % 32 == 0 && wn % 32 == 0) ? 32 : 16;
+  if (const char* e = std::getenv("LEGO_GEMM_MFMA")) MB = std::atoi(e) == 16 ? 16 : MB;
   const int KB = MB == 32 ? 16 : 32;
   if (wm % MB || wn % MB || bm % wm || bn % wn || bk % KB)
     throw Unsupported("wave tile must be a multiple of the MFMA block and divide the workgroup tile");
