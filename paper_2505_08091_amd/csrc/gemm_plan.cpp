@@ -453,6 +453,10 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
     nstages = (int)std::min<i64>(4, (160 * 1024) / stage_bytes);
     if (const char* e = std::getenv("LEGO_GEMM_STAGES")) nstages = std::atoi(e);
     nstages = (int)std::max<i64>(2, std::min<i64>(nstages, (160 * 1024) / stage_bytes));
+    // the waits count loads: NSTAGES-1 tiles behind the awaited one must fit vmcnt's 63
+    const i64 per_tile = ops[0].NV + ops[1].NV;
+    while (nstages > 2 && (nstages - 1) * per_tile > 63) --nstages;
+    if (per_tile > 63) direct = false;
   }
 
   // ----- emit the index functions

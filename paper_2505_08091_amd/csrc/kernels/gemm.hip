@@ -308,8 +308,9 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // LDS base + 16 * lane, so load vector q = u*NT + tid fills LDS slot q; the
   // planner gave that lane the global address of the logical element the LDS
   // layout puts in slot q (the inverse of the LDS layout drives the copy).
-  // NSTAGES LDS stages form a ring: the tile for step kt+NSTAGES-1 is
-  // requested at the top of step kt into the stage read during step kt-1.
+  // NSTAGES LDS stages form a ring: the tile for step kt+NSTAGES is
+  // requested during step kt, right after the barrier of its last substep,
+  // into the stage step kt has just finished reading.
   const IDX_T wu = __builtin_amdgcn_readfirstlane(tid / 64u);
 #if A_EDGE || B_EDGE
   // Range-checked buffer loads: an offset past the buffer's end (0xFFFFFFFF
@@ -354,43 +355,44 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt at their maxima).
 #define VMCNT_WAIT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | 0x70 | 0xF00)
   // Wait until at most `after` tiles of direct loads are still in flight.
+  static_assert((NSTAGES - 1) * (A_NV + B_NV) <= 63, "vmcnt counts at most 63 loads");
   auto wait_tiles = [&](int after) {
     if (after <= 0) VMCNT_WAIT(0);
-#if NSTAGES > 2
     else if (after == 1) VMCNT_WAIT(1 * (A_NV + B_NV));
-#endif
-#if NSTAGES > 3
+#if NSTAGES > 2
     else if (after == 2) VMCNT_WAIT(2 * (A_NV + B_NV));
 #endif
-#if NSTAGES > 4
-    else VMCNT_WAIT(3 * (A_NV + B_NV));
+#if NSTAGES > 3
+    else VMCNT_WAIT(3 * (A_NV + B_NV));  // (waits longer than needed beyond 3)
 #endif
   };
+  // Every stage of the ring is filled up front; afterwards the tile for step
+  // kt+NSTAGES is requested as soon as the barrier of step kt has retired the
+  // last reader of its stage (a substep before step kt+1 begins).
 #pragma unroll
-  for (int p = 0; p < NSTAGES - 1; ++p)
+  for (int p = 0; p < NSTAGES; ++p)
     if ((IDX_T)p < KT) dload(p, p);
-  wait_tiles((int)(KT - 1 < (IDX_T)(NSTAGES - 2) ? KT - 1 : (IDX_T)(NSTAGES - 2)));
+  wait_tiles((int)(KT - 1 < (IDX_T)(NSTAGES - 1) ? KT - 1 : (IDX_T)(NSTAGES - 1)));
   __syncthreads();
   fload(lds, lds + A_STAGE, 0, 0);
   for (IDX_T kt = 0; kt < KT; ++kt) {
     const int cur = kt % NSTAGES;
-    // The stage receiving tile kt+NSTAGES-1 was last read before the barrier
-    // of step kt-1.
-    if (kt + NSTAGES - 1 < KT) dload(kt + NSTAGES - 1, (kt + NSTAGES - 1) % NSTAGES);
-    __builtin_amdgcn_sched_barrier(0);
     const elem_t* la = lds + cur * STAGE;
     const elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int s = 0; s < BK / KB; ++s) {
       FRAG_WAIT();
       if (s == BK / KB - 1) {
-        // Every read of this stage has been issued.  Once tile kt+1 has landed
+        // Every read of this stage has been issued and has completed (the
+        // barrier waits for this wave's LDS reads).  Once tile kt+1 has landed
         // (tiles requested after it may stay in flight) and all waves are
-        // here, the first fragments of step kt+1 are fetched while the MFMAs
-        // of this last substep run.
+        // here, stage `cur` is free for tile kt+NSTAGES, and the first
+        // fragments of step kt+1 are fetched while the MFMAs of this last
+        // substep run.
         const IDX_T last = (kt + NSTAGES - 1 < KT ? kt + NSTAGES - 1 : KT - 1);
         wait_tiles(last > kt + 1 ? (int)(last - (kt + 1)) : 0);
         __syncthreads();
+        if (kt + NSTAGES < KT) dload(kt + NSTAGES, cur);
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
