@@ -62,7 +62,11 @@ const char* lego_version(void);
 typedef struct lego_piece_s* lego_piece_t;   /* a RegP or GenP permutation of one tile */
 typedef struct lego_layout_s* lego_layout_t; /* a GroupBy chain (or ExpandBy) */
 
-/* Release a piece or layout handle (NULL is ignored). */
+/* Handles are reference counted: a new handle holds one reference,
+ * lego_retain adds one, lego_release drops one and frees the handle with the
+ * last.  Composition keeps what it needs, so a piece may be released right
+ * after it has been composed into a layout.  NULL is ignored by both. */
+void lego_retain(void* handle);
 void lego_release(void* handle);
 
 /* ---------------------------------------------------------------- pieces --
@@ -214,9 +218,12 @@ lego_status lego_remap_plan(lego_layout_t src, lego_layout_t dst, int elem_bytes
  *         (NULL: XOR swizzle GenP with 16-byte vectors)
  * The MFMA fragment layouts are fixed by the hardware and are layouts as well
  * (see lego_mfma_fragment_layout).  xcd_remap != 0 composes a layout that keeps
- * consecutive tiles of the schedule on one XCD.  Shapes must be multiples of
- * the tile (ExpandBy edges are not supported here).  Errors: INVALID_ARG,
- * UNSUPPORTED, JIT, HIP. */
+ * consecutive tiles of the schedule on one XCD.  M, N and K need not be
+ * multiples of the tile (partial tiles, Section III-D): the tile counts round
+ * up, operand elements outside [M,K] / [K,N] load as zero and C elements
+ * outside [M,N] are not stored; operand layouts are plain (an ExpandBy
+ * operand is UNSUPPORTED).  Errors: INVALID_ARG, SIZE_MISMATCH, UNSUPPORTED,
+ * JIT, HIP. */
 enum { LEGO_F32 = 0, LEGO_F16 = 1, LEGO_BF16 = 2 };
 typedef struct {
   int64_t M, N, K;

@@ -51,6 +51,7 @@ class lego_gemm_desc(ctypes.Structure):  # noqa: N801 (C name)
 _SIGS = {
     "lego_last_error": ([], ctypes.c_char_p),
     "lego_version": ([], ctypes.c_char_p),
+    "lego_retain": ([_vp], None),
     "lego_release": ([_vp], None),
     "lego_regp": ([ctypes.c_int, c_i64p, c_i32p, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_row": ([ctypes.c_int, c_i64p, ctypes.POINTER(_vp)], ctypes.c_int),

@@ -157,6 +157,16 @@ extern "C" {
 const char* lego_last_error(void) { return g_err.c_str(); }
 const char* lego_version(void) { return "lego-mi355x 0.1 (gfx950)"; }
 
+void lego_retain(void* handle) {
+  if (!handle) return;
+  uint32_t magic;
+  std::memcpy(&magic, handle, sizeof magic);
+  if (magic == 0x50434549u)
+    ++((lego_piece_s*)handle)->rc;
+  else if (magic == 0x4c41594fu)
+    ++((lego_layout_s*)handle)->rc;
+}
+
 void lego_release(void* handle) {
   if (!handle) return;
   uint32_t magic;

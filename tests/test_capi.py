@@ -260,3 +260,19 @@ def test_jit_uses_installed_compiler(tmp_path):
     for o in objs[:3]:
         comment = subprocess.run([readelf, "-p", ".comment", str(o)], capture_output=True, text=True).stdout
         assert want in comment, (want, comment)
+
+
+def test_retain_release_reference_counts(lego):
+    """A retained handle outlives one release; the library drops it with the
+    last one (composition holds its own references)."""
+    import ctypes
+    p = lego.Row(4, 4)
+    lay = lego.as_layout(p)
+    lib = lego._lib
+    lib.lego_retain(p.h)          # two references
+    lib.lego_release(p.h)         # one left: still valid
+    d = (ctypes.c_int64 * 16)()
+    r = ctypes.c_int()
+    assert lib.lego_piece_dims(p.h, ctypes.byref(r), d) == 0 and list(d[:r.value]) == [4, 4]
+    lib.lego_retain(None)         # NULL is ignored
+    assert lay.apply([1, 2]) == 6
