@@ -181,14 +181,20 @@ def bench_gemm(L, steps, warmup):
     a = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_A).cuda()
     b = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_B).cuda()
     c = torch.empty(n * n, dtype=torch.float32, device="cuda")
-    plan = L.gemm_plan(n, n, n, "bf16")
+    # Operand and MFMA fragment layouts given explicitly as layouts (A row-major,
+    # B column-major, C row-major, the 32x32x16 fragments); the schedule and the
+    # LDS layouts are the planner's grouped + XCD order and XOR swizzles.
+    kw = dict(a=L.as_layout(L.Row(n, n)), b=L.as_layout(L.Col(n, n)), c=L.as_layout(L.Row(n, n)),
+              frag_a=L.mfma_fragment_layout(0, 0), frag_b=L.mfma_fragment_layout(0, 1),
+              frag_c=L.mfma_fragment_layout(0, 2))
+    plan = L.gemm_plan(n, n, n, "bf16", **kw)
     for _ in range(warmup):
-        L.gemm(a, b, c, n, n, n, "bf16")
+        L.gemm(a, b, c, n, n, n, "bf16", **kw)
     ev = HipEvents(steps + 1, _stream())
     torch.cuda.synchronize()
     for k in range(steps):
         ev.record(k)
-        L.gemm(a, b, c, n, n, n, "bf16")
+        L.gemm(a, b, c, n, n, n, "bf16", **kw)
     ev.record(steps)
     torch.cuda.synchronize()
     ms = ev.ms(0, steps) / steps
@@ -197,7 +203,7 @@ def bench_gemm(L, steps, warmup):
     flops = 2.0 * n ** 3
     tf = flops / (ms * 1e-3) / 1e12
     return {"ms": ms, "median_ms": _median(each), "min_ms": min(each), "tflops": tf, "plan": plan, "a": a, "b": b, "c": c,
-            "sha1": _source_sha1(L, "gemm", M=n, N=n, K=n, dtype="bf16")}
+            "sha1": _source_sha1(L, "gemm", M=n, N=n, K=n, dtype="bf16", **kw)}
 
 
 def _alternate(L, la, lb, x, y, z, reps, warmup=5):
@@ -562,7 +568,7 @@ def main():
         out["gemm"] = {
             "metric": "tiled-GEMM TFLOP/s", "value": round(g["tflops"], 1), "unit": "TFLOP/s", "dtype": "bf16",
             "workload": "bf16 GEMM M=N=K=8192, fp32 accumulation and fp32 C, A row-major, B column-major, "
-                        "256x256x64 tiles, grouped (8) + XCD schedule, XOR-swizzled LDS",
+                        "256x256x64 tiles, grouped (8) + XCD schedule, XOR-swizzled LDS, 32x32x16 MFMA fragment layouts given as layouts",
             "plan": g["plan"], "steps": args.gemm_steps, "warmup": args.gemm_warmup,
             "roofline": {"bound": "mfma", "achieved": round(g["tflops"], 1), "peak": BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(g["tflops"] / BF16_PEAK_TFLOPS, 4),

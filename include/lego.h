@@ -216,8 +216,13 @@ lego_status lego_remap_plan(lego_layout_t src, lego_layout_t dst, int elem_bytes
  *         a group, the order the paper's Triton matmul uses)
  *   lds_a over [bm, bk] and lds_b over [bn, bk]: element offsets in the LDS tile
  *         (NULL: XOR swizzle GenP with 16-byte vectors)
- * The MFMA fragment layouts are fixed by the hardware and are layouts as well
- * (see lego_mfma_fragment_layout).  xcd_remap != 0 composes a layout that keeps
+ * frag_a, frag_b, frag_c: the register fragment layouts of the MFMA
+ *         instruction, as lego_mfma_fragment_layout returns them (logical
+ *         (lane, element) -> position in the A, B or C block).  The hardware
+ *         fixes them per instruction, so given layouts select the instruction
+ *         (32x32x16 or 16x16x32) whose fragments they are, compared point by
+ *         point; layouts of no instruction, or of different ones, are
+ *         UNSUPPORTED.  NULL: 32x32x16 when the wave tile allows it.  xcd_remap != 0 composes a layout that keeps
  * consecutive tiles of the schedule on one XCD.  M, N and K need not be
  * multiples of the tile (partial tiles, Section III-D): the tile counts round
  * up, operand elements outside [M,K] / [K,N] load as zero and C elements
@@ -233,6 +238,7 @@ typedef struct {
   int group_m;           /* grouping of the default schedule; 0 = 8 */
   int xcd_remap;         /* 1 = keep consecutive scheduled tiles on one XCD */
   lego_layout_t a, b, c, sched, lds_a, lds_b;
+  lego_layout_t frag_a, frag_b, frag_c;  /* MFMA fragment layouts (see below); NULL: chosen */
 } lego_gemm_desc;
 lego_status lego_gemm(const lego_gemm_desc* desc, const void* d_a, const void* d_b, float* d_c, void* stream);
 

@@ -45,7 +45,8 @@ class lego_gemm_desc(ctypes.Structure):  # noqa: N801 (C name)
     _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
                 ("in_dtype", ctypes.c_int), ("bm", ctypes.c_int), ("bn", ctypes.c_int), ("bk", ctypes.c_int),
                 ("wm", ctypes.c_int), ("wn", ctypes.c_int), ("group_m", ctypes.c_int), ("xcd_remap", ctypes.c_int),
-                ("a", _vp), ("b", _vp), ("c", _vp), ("sched", _vp), ("lds_a", _vp), ("lds_b", _vp)]
+                ("a", _vp), ("b", _vp), ("c", _vp), ("sched", _vp), ("lds_a", _vp), ("lds_b", _vp),
+                ("frag_a", _vp), ("frag_b", _vp), ("frag_c", _vp)]
 
 
 _SIGS = {
@@ -337,12 +338,13 @@ def remap_plan(src_layout, dst_layout, elem_bytes):
 
 
 def _desc(M, N, K, dtype, a=None, b=None, c=None, sched=None, lds_a=None, lds_b=None, bm=0, bn=0, bk=0, wm=0, wn=0,
-          group_m=0, xcd_remap=1):
+          group_m=0, xcd_remap=1, frag_a=None, frag_b=None, frag_c=None):
     d = lego_gemm_desc()
     d.M, d.N, d.K = int(M), int(N), int(K)
     d.in_dtype = DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
     d.bm, d.bn, d.bk, d.wm, d.wn, d.group_m, d.xcd_remap = bm, bn, bk, wm, wn, group_m, xcd_remap
-    for name, lay in (("a", a), ("b", b), ("c", c), ("sched", sched), ("lds_a", lds_a), ("lds_b", lds_b)):
+    for name, lay in (("a", a), ("b", b), ("c", c), ("sched", sched), ("lds_a", lds_a), ("lds_b", lds_b),
+                      ("frag_a", frag_a), ("frag_b", frag_b), ("frag_c", frag_c)):
         setattr(d, name, lay.h if lay is not None else None)
     return d
 

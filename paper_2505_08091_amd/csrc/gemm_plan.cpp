@@ -47,12 +47,32 @@ GemmRequest gemm_request(const lego_gemm_desc& d, const std::function<LayoutP(le
   r.sched = resolve(d.sched);
   r.lds_a = resolve(d.lds_a);
   r.lds_b = resolve(d.lds_b);
+  r.frag_a = resolve(d.frag_a);
+  r.frag_b = resolve(d.frag_b);
+  r.frag_c = resolve(d.frag_c);
   return r;
 }
 
 namespace {
 
 bool pow2(i64 x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// Two layouts with equal dims and sizes that map every logical point alike.
+bool same_map(const Layout& x, const Layout& y) {
+  if (x.dims() != y.dims() || x.size() != y.size()) return false;
+  const std::vector<i64> n = x.dims();
+  std::vector<i64> idx(n.size(), 0);
+  IntAlg al;
+  for (i64 f = 0; f < x.size(); ++f) {
+    i64 r = f;
+    for (size_t k = n.size(); k-- > 0;) {
+      idx[k] = r % n[k];
+      r /= n[k];
+    }
+    if (x.apply(al, idx) != y.apply(al, idx)) return false;
+  }
+  return true;
+}
 
 // Default LDS tile layout: 16-byte vectors of a row XOR-permuted by (row/s)
 // mod (k/8).  A b128 fragment read is served 16 lanes (16 rows) at a time over
@@ -152,6 +172,21 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   const bool edge_m = M % bm != 0, edge_n = N % bn != 0, edge_k = K % bk != 0;
   int MB = (wm % 32 == 0 && wn % 32 == 0) ? 32 : 16;
   if (const char* e = std::getenv("LEGO_GEMM_MFMA")) MB = std::atoi(e) == 16 ? 16 : MB;
+  {
+    // Given fragment layouts select the instruction whose fragments they are.
+    int want = -1;
+    const LayoutP given[3] = {rq.frag_a, rq.frag_b, rq.frag_c};
+    for (int op = 0; op < 3; ++op) {
+      if (!given[op]) continue;
+      int match = -1;
+      for (int instr = 0; instr < 2 && match < 0; ++instr)
+        if (same_map(*given[op], *mfma_fragment_layout(instr, op))) match = instr;
+      if (match < 0) throw Unsupported("fragment layout is not the fragment layout of a supported MFMA instruction");
+      if (want >= 0 && want != match) throw Unsupported("fragment layouts of different MFMA instructions");
+      want = match;
+    }
+    if (want >= 0) MB = want == 0 ? 32 : 16;
+  }
   const int KB = MB == 32 ? 16 : 32;
   if (wm % MB || wn % MB || bm % wm || bn % wn || bk % KB)
     throw Unsupported("wave tile must be a multiple of the MFMA block and divide the workgroup tile");
@@ -773,7 +808,8 @@ std::shared_ptr<GemmPlan> gemm_plan_cached(const GemmRequest& rq) {
   std::ostringstream k;
   k << rq.M << "," << rq.N << "," << rq.K << "," << rq.dtype << "," << rq.bm << "," << rq.bn << "," << rq.bk << ","
     << rq.wm << "," << rq.wn << "," << rq.group_m << "," << rq.xcd;
-  for (auto* l : {&rq.a, &rq.b, &rq.c, &rq.sched, &rq.lds_a, &rq.lds_b}) k << "," << (const void*)l->get();
+  for (auto* l : {&rq.a, &rq.b, &rq.c, &rq.sched, &rq.lds_a, &rq.lds_b, &rq.frag_a, &rq.frag_b, &rq.frag_c})
+    k << "," << (const void*)l->get();
   std::string key = k.str();
   {
     std::lock_guard<std::mutex> lk(g_mu);
@@ -782,7 +818,7 @@ std::shared_ptr<GemmPlan> gemm_plan_cached(const GemmRequest& rq) {
   }
   auto p = std::make_shared<GemmPlan>(plan_gemm(rq));
   std::lock_guard<std::mutex> lk(g_mu);
-  g_cache[key] = {{rq.a, rq.b, rq.c, rq.sched, rq.lds_a, rq.lds_b}, p};
+  g_cache[key] = {{rq.a, rq.b, rq.c, rq.sched, rq.lds_a, rq.lds_b, rq.frag_a, rq.frag_b, rq.frag_c}, p};
   return p;
 }
 

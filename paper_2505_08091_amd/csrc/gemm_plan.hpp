@@ -19,6 +19,7 @@ struct GemmRequest {
   int dtype = LEGO_BF16;
   int bm = 0, bn = 0, bk = 0, wm = 0, wn = 0, group_m = 0, xcd = 0;
   LayoutP a, b, c, sched, lds_a, lds_b;  // null: defaults
+  LayoutP frag_a, frag_b, frag_c;        // null: chosen; else they select the MFMA instruction
 };
 
 struct GemmPlan : KernelPlan {};

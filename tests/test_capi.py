@@ -276,3 +276,20 @@ def test_retain_release_reference_counts(lego):
     assert lib.lego_piece_dims(p.h, ctypes.byref(r), d) == 0 and list(d[:r.value]) == [4, 4]
     lib.lego_retain(None)         # NULL is ignored
     assert lay.apply([1, 2]) == 6
+
+
+def test_fragment_layouts_select_instruction_on_host(lego):
+    """frag_a/b/c given as the hardware's fragment layouts choose the MFMA
+    instruction; mixed or foreign layouts are UNSUPPORTED; giving the default
+    instruction's layouts generates the default kernel source."""
+    f = [[lego.mfma_fragment_layout(i, op) for op in range(3)] for i in range(2)]
+    p32 = lego.gemm_plan(1024, 1024, 1024, "bf16", frag_a=f[0][0], frag_b=f[0][1], frag_c=f[0][2])
+    p16 = lego.gemm_plan(1024, 1024, 1024, "bf16", frag_c=f[1][2])
+    assert "mfma 32x32x16" in p32 and "mfma 16x16x32" in p16
+    assert lego.plan_source("gemm", M=1024, N=1024, K=1024, dtype="bf16", frag_a=f[0][0]) == \
+        lego.plan_source("gemm", M=1024, N=1024, K=1024, dtype="bf16")
+    for bad in (dict(frag_a=f[0][0], frag_c=f[1][2]), dict(frag_c=lego.as_layout(lego.Row(64, 16))),
+                dict(frag_b=lego.as_layout(lego.Row(64, 8)))):
+        with pytest.raises(lego.LegoError) as e:
+            lego.gemm_plan(1024, 1024, 1024, "bf16", **bad)
+        assert e.value.status == "UNSUPPORTED"

@@ -88,6 +88,25 @@ def test_gemm_layout_variants(lego):
             assert ok, (la_name, lb_name, mre, fre)
 
 
+@pytest.mark.parametrize("instr", [0, 1])
+def test_gemm_fragment_layouts_select_the_instruction(lego, instr):
+    """The MFMA fragment layouts given as layouts (frag_a/b/c) pick the
+    instruction: 32x32x16 (0) or 16x16x32 (1), on a 1024x768x512 bf16 GEMM."""
+    M, N, K = 1024, 768, 512
+    a = S.tensor(M * K, "bf16", dist="normal", seed=S.SEED_A)
+    b = S.tensor(K * N, "bf16", dist="normal", seed=S.SEED_B)
+    kw = dict(frag_a=lego.mfma_fragment_layout(instr, 0), frag_b=lego.mfma_fragment_layout(instr, 1),
+              frag_c=lego.mfma_fragment_layout(instr, 2))
+    plan = lego.gemm_plan(M, N, K, "bf16", **kw)
+    say(f"gemm fragments instr {instr} plan={plan}")
+    assert ("mfma 32x32x16" if instr == 0 else "mfma 16x16x32") in plan
+    c = _run(lego, a, b, M, N, K, "bf16", **kw).reshape(M, N)
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(OL.Row(M, K)), OL.as_layout(OL.Col(K, N)),
+                "bf16")
+    ok, mre, fre = OG.check_tolerance(c, r)
+    assert ok, (mre, fre)
+
+
 def test_gemm_fragment_probe_one_hot(lego):
     """A = e_(m,k), B = e_(k,n): C must be exactly 1 at (m, n) and 0 elsewhere,
     which pins the C/D fragment layout of the MFMA instruction."""
