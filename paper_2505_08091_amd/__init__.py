@@ -109,10 +109,26 @@ def _i64(xs):
     return (ctypes.c_int64 * max(1, len(xs)))(*xs)
 
 
+_RAW_STREAM = None
+
+
+def _current_stream():
+    """torch's current HIP stream on the current device (the raw lookup costs
+    a fraction of a microsecond; torch.cuda.current_stream() several)."""
+    global _RAW_STREAM
+    if _RAW_STREAM is None:
+        import torch
+        get, dev = getattr(torch._C, "_cuda_getCurrentRawStream", None), getattr(torch._C, "_cuda_getDevice", None)
+        if get is not None and dev is not None:
+            _RAW_STREAM = lambda: get(dev())  # noqa: E731
+        else:
+            _RAW_STREAM = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+    return _RAW_STREAM()
+
+
 def _stream(stream):
     if stream is None:
-        import torch
-        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        return ctypes.c_void_p(_current_stream())
     if isinstance(stream, int):
         return ctypes.c_void_p(stream)
     return ctypes.c_void_p(stream.cuda_stream)

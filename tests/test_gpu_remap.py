@@ -238,3 +238,23 @@ def test_remap_errors(lego):
     with pytest.raises(lego.LegoError) as e:
         lego.remap(r, r, a, a)
     assert e.value.status == "INVALID_ARG"
+
+
+def test_binding_follows_torch_current_stream(lego):
+    """The binding launches on torch's current stream: the default one and a
+    side stream entered with torch.cuda.stream (then the result is ordered
+    after that stream's earlier work)."""
+    import torch
+    dev = need_gpu()
+    assert (lego._stream(None).value or 0) == torch.cuda.current_stream().cuda_stream
+    side = torch.cuda.Stream()
+    n = 1024
+    row, col = lego.as_layout(lego.Row(n, n)), lego.as_layout(lego.Col(n, n))
+    src = S.tensor(n * n, "f32", seed=S.SEED_SRC)
+    with torch.cuda.stream(side):
+        assert lego._stream(None).value == side.cuda_stream
+        x = src.to(dev, non_blocking=False)
+        y = torch.empty_like(x)
+        lego.remap(row, col, x, y)
+    side.synchronize()
+    assert (bits(y.cpu()) == bits(src).reshape(n, n).T.ravel()).all()
