@@ -318,11 +318,13 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)A_BYTES, 0x00020000);
   const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)B, (short)0, (int)B_BYTES, 0x00020000);
 #endif
-  auto dload = [&](IDX_T kt, int stage) {
+  // Copies [lo, hi) of the tile for step kt (A's A_NV vectors, then B's).
+  auto dload_part = [&](IDX_T kt, int stage, int lo, int hi) {
     elem_t* la = lds + stage * STAGE;
     elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
+      if (u < lo || u >= hi) continue;
 #if A_SEP
       const elem_t* src = Ab + a_gk(kt) + a_loc[u];
 #else
@@ -338,6 +340,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     }
 #pragma unroll
     for (int u = 0; u < B_NV; ++u) {
+      if (A_NV + u < lo || A_NV + u >= hi) continue;
 #if B_SEP
       const elem_t* src = Bb + b_gk(kt) + b_loc[u];
 #else
@@ -352,6 +355,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #endif
     }
   };
+  auto dload = [&](IDX_T kt, int stage) { dload_part(kt, stage, 0, A_NV + B_NV); };
   // s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt at their maxima).
 #define VMCNT_WAIT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | 0x70 | 0xF00)
   // Wait until at most `after` tiles of direct loads are still in flight.
@@ -392,9 +396,25 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         const IDX_T last = (kt + NSTAGES - 1 < KT ? kt + NSTAGES - 1 : KT - 1);
         wait_tiles(last > kt + 1 ? (int)(last - (kt + 1)) : 0);
         __syncthreads();
-        if (kt + NSTAGES < KT) dload(kt + NSTAGES, cur);
         __builtin_amdgcn_sched_barrier(0);
       }
+#if DMA_SPREAD
+      if (s == BK / KB - 1) {
+        // The copies of tile kt+NSTAGES go out between the rows of MFMAs, a
+        // share after each row, so the matrix pipe is never left idle while
+        // the wave issues a burst of them.
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+#pragma unroll
+          for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+          __builtin_amdgcn_sched_barrier(0);
+          if (kt + NSTAGES < KT) dload_part(kt + NSTAGES, cur, i * (A_NV + B_NV) / MI, (i + 1) * (A_NV + B_NV) / MI);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else
+#else
+      if (s == BK / KB - 1 && kt + NSTAGES < KT) dload(kt + NSTAGES, cur);
+#endif
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
