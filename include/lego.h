@@ -183,6 +183,7 @@ lego_status lego_emit(lego_layout_t l, int which, char* buf, size_t cap, size_t*
  * apply_all: d_out[x] = apply(B^{-1}(x)) for every logical flat x, idx_bytes
  *   = 4 (int32) or 8 (int64); d_out holds size elements.
  * inv_all: d_out[p*rank + k] = inv(p)[k] for every physical p.
+ * d_out must be 16-byte aligned (the kernels store 16-byte vectors).
  * Errors: INVALID_ARG, JIT, HIP. */
 lego_status lego_apply_all_device(lego_layout_t l, int idx_bytes, void* d_out, void* stream);
 lego_status lego_inv_all_device(lego_layout_t l, int idx_bytes, void* d_out, void* stream);
@@ -227,8 +228,9 @@ lego_status lego_remap_plan(lego_layout_t src, lego_layout_t dst, int elem_bytes
  * multiples of the tile (partial tiles, Section III-D): the tile counts round
  * up, operand elements outside [M,K] / [K,N] load as zero and C elements
  * outside [M,N] are not stored; operand layouts are plain (an ExpandBy
- * operand is UNSUPPORTED).  Errors: INVALID_ARG, SIZE_MISMATCH, UNSUPPORTED,
- * JIT, HIP. */
+ * operand is UNSUPPORTED).  d_a and d_b must be 16-byte aligned, d_c 4-byte
+ * aligned, and C must not overlap A or B (INVALID_ARG).  Errors: INVALID_ARG,
+ * SIZE_MISMATCH, UNSUPPORTED, JIT, HIP. */
 enum { LEGO_F32 = 0, LEGO_F16 = 1, LEGO_BF16 = 2 };
 typedef struct {
   int64_t M, N, K;

@@ -386,6 +386,7 @@ lego_status lego_apply_all_device(lego_layout_t l, int idx_bytes, void* d_out, v
   return guard([&] {
     auto lay = layout_of(l);
     if (!d_out) throw std::invalid_argument("null device pointer");
+    if ((uintptr_t)d_out & 15) throw std::invalid_argument("output must be 16-byte aligned");
     auto plan = cached_plan(lay, nullptr, 100, idx_bytes, [&] {
       return std::make_shared<KernelPlan>(plan_index_eval(*lay, 0, idx_bytes));
     });
@@ -399,6 +400,7 @@ lego_status lego_inv_all_device(lego_layout_t l, int idx_bytes, void* d_out, voi
   return guard([&] {
     auto lay = layout_of(l);
     if (!d_out) throw std::invalid_argument("null device pointer");
+    if ((uintptr_t)d_out & 15) throw std::invalid_argument("output must be 16-byte aligned");
     auto plan = cached_plan(lay, nullptr, 101, idx_bytes, [&] {
       return std::make_shared<KernelPlan>(plan_index_eval(*lay, 1, idx_bytes));
     });
@@ -486,6 +488,17 @@ lego_status lego_gemm(const lego_gemm_desc* desc, const void* d_a, const void* d
   return guard([&] {
     if (!desc || !d_a || !d_b || !d_c) throw std::invalid_argument("null pointer");
     GemmRequest rq = gemm_request(*desc, [](lego_layout_t h) { return h ? layout_of(h) : LayoutP(); });
+    // The operands are read with 16-byte vectors; C is written element by element.
+    if (((uintptr_t)d_a | (uintptr_t)d_b) & 15) throw std::invalid_argument("A and B must be 16-byte aligned");
+    if ((uintptr_t)d_c & 3) throw std::invalid_argument("C must be 4-byte aligned");
+    if (rq.M > 0 && rq.N > 0 && rq.K > 0) {
+      auto bytes = [](const LayoutP& l, i64 n, i64 eb) { return (l ? l->phys_size() : n) * eb; };
+      const i64 ab = bytes(rq.a, rq.M * rq.K, 2), bb = bytes(rq.b, rq.K * rq.N, 2), cb = bytes(rq.c, rq.M * rq.N, 4);
+      auto overlap = [](const void* x, i64 xn, const void* y, i64 yn) {
+        return (const char*)x < (const char*)y + yn && (const char*)y < (const char*)x + xn;
+      };
+      if (overlap(d_c, cb, d_a, ab) || overlap(d_c, cb, d_b, bb)) throw std::invalid_argument("C overlaps A or B");
+    }
     std::shared_ptr<GemmPlan> plan = gemm_plan_cached(rq);
     void* a = const_cast<void*>(d_a);
     void* b = const_cast<void*>(d_b);

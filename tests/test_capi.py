@@ -293,3 +293,26 @@ def test_fragment_layouts_select_instruction_on_host(lego):
         with pytest.raises(lego.LegoError) as e:
             lego.gemm_plan(1024, 1024, 1024, "bf16", **bad)
         assert e.value.status == "UNSUPPORTED"
+
+
+def test_gemm_argument_checks_before_any_device_work(lego):
+    """Misaligned operands and a C that overlaps A or B are refused with
+    INVALID_ARG before the library plans or launches anything (the pointers
+    here are never dereferenced)."""
+    import ctypes
+    M = N = K = 256
+    d = lego._desc(M, N, K, "f16")
+    base = 1 << 20
+    a, b, c = base, base + 2 * M * K, base + 4 * M * K
+    cases = [(a + 8, b, c), (a, b + 2, c), (a, b, c + 2), (a, b, a + 1024), (a, b, b - 16)]
+    for pa, pb, pc in cases:
+        rc = lego._lib.lego_gemm(ctypes.byref(d), ctypes.c_void_p(pa), ctypes.c_void_p(pb), ctypes.c_void_p(pc), None)
+        assert rc == -1, (pa, pb, pc, rc)
+
+
+def test_index_map_output_alignment_checked(lego):
+    """A device output that is not 16-byte aligned is refused before any launch."""
+    import ctypes
+    lay = lego.as_layout(lego.Row(8, 8))
+    for f in (lego._lib.lego_apply_all_device, lego._lib.lego_inv_all_device):
+        assert f(lay.h, 4, ctypes.c_void_p((1 << 20) + 4), None) == -1
