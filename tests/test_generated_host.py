@@ -466,13 +466,16 @@ def _gemm_cases():
                           b=L.as_layout(getattr(L, lb)(2048, 2048))))
     from tests.test_gpu_gemm import _ragged_cases
     cases += [{k: v for k, v in c.items() if k not in ("oa", "ob")} for c in _ragged_cases(L)]
+    from tests.test_gpu_gemm import _sched_cases
+    for _, sched, xcd in _sched_cases(L, 8, 8):
+        cases.append(dict(M=2048, N=2048, K=512, dtype="bf16", sched=sched, xcd_remap=xcd))
     from tests import genp_exprs as GE
     sw = L.as_layout(L.GenPExpr([256, 64], GE.SWIZZLE64_APPLY, GE.SWIZZLE64_INV))
     cases.append(dict(M=1024, N=1024, K=1024, dtype="bf16", lds_a=sw, lds_b=sw))
     return cases
 
 
-@pytest.mark.parametrize("i", range(28))
+@pytest.mark.parametrize("i", range(34))
 def test_gemm_sources_of_gpu_cases(i):
     import paper_2505_08091_amd as L
     cases = _gemm_cases()

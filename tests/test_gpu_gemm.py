@@ -129,6 +129,32 @@ def test_gemm_one_wave_per_simd(lego, staged):
     assert ok, (mre, fre)
 
 
+def _sched_cases(L, mt, nt):
+    """Workgroup schedules given as layouts over the [Mt, Nt] tile grid: tile
+    (tm, tn) is computed by workgroup sched.apply(tm, tn)."""
+    return [("row-major tile order", L.as_layout(L.Row(mt, nt)), 0),
+            ("row-major tile order, XCD remap", L.as_layout(L.Row(mt, nt)), 1),
+            ("column-major tile order", L.as_layout(L.Col(mt, nt)), 1),
+            ("groups of 4 tile rows, as a chain", L.GroupBy([mt, nt]).OrderBy(L.RegP([mt // 4, 4, nt], [1, 3, 2])), 1),
+            ("Morton tile order", L.as_layout(L.GenP("morton", [mt, nt])), 1)]
+
+
+def test_gemm_user_schedules(lego):
+    """GEMMs whose workgroup order is a user-given layout (Section II's
+    grouped order is one such layout) against the oracle: the schedule moves
+    work between workgroups but never changes C."""
+    M, N, K = 2048, 2048, 512
+    a = S.tensor(M * K, "bf16", dist="normal", seed=S.SEED_A)
+    b = S.tensor(K * N, "bf16", dist="normal", seed=S.SEED_B)
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(OL.Row(M, K)), OL.as_layout(OL.Col(K, N)),
+                "bf16")
+    for name, sched, xcd in _sched_cases(lego, M // 256, N // 256):
+        say(f"gemm schedule {name} plan={lego.gemm_plan(M, N, K, 'bf16', sched=sched, xcd_remap=xcd)}")
+        c = _run(lego, a, b, M, N, K, "bf16", sched=sched, xcd_remap=xcd).reshape(M, N)
+        ok, mre, fre = OG.check_tolerance(c, r)
+        assert ok, (name, mre, fre)
+
+
 def test_gemm_fragment_probe_one_hot(lego):
     """A = e_(m,k), B = e_(k,n): C must be exactly 1 at (m, n) and 0 elsewhere,
     which pins the C/D fragment layout of the MFMA instruction."""
