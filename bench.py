@@ -276,7 +276,8 @@ def bench_extra(L, reps=20):
     the 2D transpose of Section V-C), Row <-> Morton fp16 4096^2 hot and with
     the last-level cache flushed, the 4096^3 fp16 GEMM with A in Morton order
     and B row-major, the four Row/Col operand layouts of an 8192^3 fp16 GEMM
-    (Section V-A), partial tiles: a padding/cropping remap and an 8000^3
+    (Section V-A), workgroup schedules given as layouts (grouped, row-major,
+    Morton; Section II), partial tiles: a padding/cropping remap and an 8000^3
     GEMM (Section III-D), 3-D bricks of a 512^3 grid, and user-defined GenPs from expression text: a
     wavefront tile order and an LDS swizzle (Section III-B)."""
     import torch
@@ -376,6 +377,23 @@ def bench_extra(L, reps=20):
             ms = _gemm_ms(L, a, b, c, n, "f16", 20, **kw)
             var[f"A {la} B {lb}"] = round(2.0 * n ** 3 / (ms * 1e-3) / 1e12, 1)
     out["gemm_operand_layouts_f16_8192_tflops"] = var
+    del a, b, c
+
+    # Workgroup schedules given as layouts over the 32 x 32 tile grid of the
+    # 8192^3 bf16 GEMM (Section II: the grouped order against row-major).
+    a = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_A).cuda()
+    b = S.tensor(n * n, "bf16", dist="normal", seed=S.SEED_B).cuda()
+    c = torch.empty(n * n, dtype=torch.float32, device="cuda")
+    t = n // 256
+    sch = {}
+    for name, kw in (("grouped 8 + XCD remap (default)", {}),
+                     ("grouped 8", dict(xcd_remap=0)),
+                     ("row-major", dict(sched=L.as_layout(L.Row(t, t)), xcd_remap=0)),
+                     ("row-major + XCD remap", dict(sched=L.as_layout(L.Row(t, t)))),
+                     ("Morton", dict(sched=L.as_layout(L.GenP("morton", [t, t])), xcd_remap=0))):
+        ms = _gemm_ms(L, a, b, c, n, "bf16", 20, **kw)
+        sch[name] = round(2.0 * n ** 3 / (ms * 1e-3) / 1e12, 1)
+    out["gemm_schedules_bf16_8192_tflops"] = sch
     del a, b, c
 
     # Partial tiles (ExpandBy, Section III-D): an 8000 x 8000 fp32 array into a
