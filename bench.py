@@ -422,6 +422,20 @@ def bench_extra(L, reps=20):
                                     "plan": L.gemm_plan(n, n, n, "bf16")}
     del a, b, c
 
+    # A whole 4096^2 fp32 matrix in antidiagonal order (Figure 7's GenP, the
+    # wavefront order of Section V's NW example) and back: no digit structure,
+    # so an element gather.
+    n = 4096
+    x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()
+    y, z = torch.empty_like(x), torch.empty_like(x)
+    row, ad = L.as_layout(L.Row(n, n)), L.as_layout(L.GenP("antidiag", [n, n]))
+    f, i = _alternate(L, row, ad, x, y, z, reps)
+    nb = 2 * n * n * 4
+    out["antidiagonal_f32_4096"] = {"bytes_per_launch": nb, "row_to_antidiag_GBps": gbps(nb, f),
+                                    "antidiag_to_row_GBps": gbps(nb, i),
+                                    "plan": L.remap_plan(row, ad, 4)["info"]}
+    del x, y, z
+
     # 3-D bricks (the stencil data layout of Section V): a 512^3 fp32 grid
     # between row-major order and bricks of 8^3 or 4^3 elements stored
     # contiguously, bricks in row-major order.

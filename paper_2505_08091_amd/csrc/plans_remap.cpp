@@ -249,8 +249,10 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   // fastest for HBM-resident tensors that are not reused by the same kernel,
   // both with caches cleaned between launches and when a remap consumes the
   // previous remap's output; cached stores leave that output in the last-level
-  // cache for its consumer.
-  int nontemporal = 1;
+  // cache for its consumer.  An element gather reads each source line many
+  // times over neighbouring chunks, so its loads stay cached (Row <->
+  // antidiagonal 4096^2 fp32: 0.74/0.97 -> 1.11/1.78 TB/s).
+  int nontemporal = R.path == REMAP_GATHER ? 0 : 1;
   if (const char* e = std::getenv("LEGO_REMAP_NONTEMPORAL")) nontemporal = std::atoi(e);
   if (R.path == REMAP_DIRECT || R.path == REMAP_GATHER) {
     // 8 vectors in flight per thread (a 32 KiB chunk per workgroup at 16-byte
@@ -315,10 +317,20 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
       }
       std::sort(cd.begin(), cd.end(), [](const Dg& x, const Dg& y) { return x.c < y.c; });
     }
+    // In destination order, workgroups are dispatched round-robin over the 8
+    // XCDs (each with its own L2): an element gather gives XCD x the x-th
+    // eighth of the chunks, so neighbouring chunks, which such a map reads
+    // from neighbouring source lines, share one L2.
+    // (Measured on the element-gather path: Row <-> antidiagonal 4096^2 fp32
+    // 0.42/0.63 -> 0.74/0.98 TB/s; vector maps gain nothing from it.)
+    bool xcd_blocks = !src_order && !pure && nblk % 8 == 0 && R.path == REMAP_GATHER;
+    if (const char* e = std::getenv("LEGO_REMAP_XCD")) xcd_blocks = xcd_blocks && std::atoi(e) != 0;
     std::vector<std::pair<std::string, std::function<FnSpec(Ctx&)>>> dfns = {{"blk",
                                  [&](Ctx& c) {
                                    int b = c.var("b", nblk);
                                    Sum o = var(c, b);
+                                   if (xcd_blocks)
+                                     o = add(c, mulc(c, fmod(c, var(c, b), 8), nblk / 8), fdiv(c, var(c, b), 8));
                                    if (src_order) {
                                      o = cst(0);
                                      i64 w = 1;
@@ -384,7 +396,8 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     R.vec = V;
     R.vec_dst = V;
     R.src = s.str();
-    R.info = std::string(R.path == REMAP_DIRECT ? "direct" : "gather") + (src_order ? " src-order" : " dst-order") +
+    R.info = std::string(R.path == REMAP_DIRECT ? "direct" : "gather") +
+             (src_order ? " src-order" : (xcd_blocks ? " dst-order-xcd" : " dst-order")) +
              " NT=" + std::to_string(NT) + " UNROLL=" + std::to_string(UNROLL) + " V=" + std::to_string(V) +
              (src_sep ? " chunk-base" : "") +
              " run=" + std::to_string(run) + (masked ? " masked" : "") + info;
