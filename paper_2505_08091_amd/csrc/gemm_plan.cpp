@@ -143,7 +143,11 @@ struct Operand {
 
 }  // namespace
 
-GemmPlan plan_gemm(const GemmRequest& rq0) {
+namespace {
+
+// `wide_waves`: the default wave tile of a 256-wide workgroup tile is 128
+// wide (else 64) along n.
+GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   GemmRequest rq = rq0;
   if (rq.dtype != LEGO_F16 && rq.dtype != LEGO_BF16) throw std::invalid_argument("GEMM inputs must be fp16 or bf16");
   if (rq.M <= 0 || rq.N <= 0 || rq.K <= 0) throw std::invalid_argument("GEMM sizes must be positive");
@@ -158,10 +162,11 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   if (!rq.bm) rq.bm = pick(rq.M);
   if (!rq.bn) rq.bn = pick(rq.N);
   if (!rq.bk) rq.bk = rq.K >= 64 ? 64 : 32;
-  // Default wave tiles keep at most 8 MFMA blocks (128 fp32 accumulators) per
-  // wave, so accumulators stay in VGPRs and two waves share each SIMD.
-  if (!rq.wm) rq.wm = rq.bm >= 256 ? 128 : (rq.bm >= 64 ? rq.bm / 2 : rq.bm);
-  if (!rq.wn) rq.wn = rq.bn >= 256 ? 64 : (rq.bn >= 64 ? rq.bn / 2 : rq.bn);
+  // Default wave tiles: half the workgroup tile each way (2x2 waves), but at
+  // most 64 wide along n for a 256-wide tile unless `wide_waves` (then 128x128
+  // wave tiles whose 256 fp32 accumulators fill the AGPRs, one wave per SIMD).
+  if (!rq.wm) rq.wm = rq.bm >= 64 ? rq.bm / 2 : rq.bm;
+  if (!rq.wn) rq.wn = rq.bn >= 256 && !wide_waves ? 64 : (rq.bn >= 64 ? rq.bn / 2 : rq.bn);
   if (!rq.group_m) rq.group_m = 8;
   const i64 M = rq.M, N = rq.N, K = rq.K;
   const int bm = rq.bm, bn = rq.bn, bk = rq.bk, wm = rq.wm, wn = rq.wn;
@@ -769,13 +774,23 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
   // tile in one substep.
   int rolling = 1;
   if (const char* e = std::getenv("LEGO_GEMM_ROLLING")) rolling = std::atoi(e) != 0;
-  // With one wave per SIMD the direct copies of the next tile go out between
-  // the MFMA rows of the last substep (measured 0.87 -> 0.85 ms on the 8192^3
-  // bf16 GEMM with 128x128 wave tiles); with two waves a burst costs nothing.
-  int dma_spread = MI * NI * NREG > 128 ? 1 : 0;
+  // The direct copies of the next tile go out between MFMA rows rather than
+  // in one burst (measured 0.87 -> 0.85 ms on the 8192^3 bf16 GEMM with
+  // 128x128 wave tiles, and 0.870 -> 0.864 ms with 8 waves of 128x64).
+  int dma_spread = 1;
   if (const char* e = std::getenv("LEGO_GEMM_DMA_SPREAD")) dma_spread = std::atoi(e) != 0;
+  // Direct-copy plans read fragments two substeps ahead of their MFMAs, so
+  // that reads held up by copies landing in LDS do not stall them (0.857 ->
+  // 0.852 ms on the 8192^3 bf16 GEMM); not with the transposing reads, whose
+  // wait at each substep covers every read in flight.
+  int frag_dist = (ops[0].frtr || ops[1].frtr) ? 1 : 2;
+  if (const char* e = std::getenv("LEGO_GEMM_FRAG_DIST")) frag_dist = std::max(1, std::min(2, std::atoi(e)));
+  // (Reads two substeps ahead need three substeps per step: with two, the
+  // early reads of the last substep would replace fragments its later MFMA
+  // rows still use.)
+  if (!direct || bk / KB <= frag_dist) frag_dist = 1;
   s << "#define PREFETCH " << prefetch << "\n#define ROLLING " << rolling << "\n#define DMA_SPREAD " << dma_spread
-    << "\n#define DIRECT_LDS " << (direct ? 1 : 0)
+    << "\n#define FRAG_DIST " << frag_dist << "\n#define DIRECT_LDS " << (direct ? 1 : 0)
     << "\n#define NSTAGES " << nstages << "\n";
   const char* store_env = std::getenv("LEGO_GEMM_STORE_AT");
   int store_at = store_env ? std::atoi(store_env) : (bk / KB) / 2;
@@ -798,11 +813,27 @@ GemmPlan plan_gemm(const GemmRequest& rq0) {
        << (ops[1].gaxis == 2 ? "b" + std::to_string(ops[1].VR) + "x" + std::to_string(ops[1].VC) : (ops[1].gaxis ? "k" : "n"))
        << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
        << (ops[1].frvec ? " frvec" : (ops[1].frtr ? " frtr" : " frscalar")) << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
-       << (direct ? " direct-lds" : " staged") << (ragged_groups ? " ragged-groups" : "")
+       << (direct ? " direct-lds" : " staged")
+       << (direct ? std::string(dma_spread ? " spread" : " burst") + " fd" + std::to_string(frag_dist) : "")
+       << (ragged_groups ? " ragged-groups" : "")
        << (ops[0].edge || ops[1].edge || cedge ? " edges" : "") << " stages " << nstages << " lds " << nstages * stage_bytes
        << "B ops" << opsinfo.str();
   g.info = info.str();
+  g.direct_vec = direct && ops[0].frvec && ops[1].frvec;
   return g;
+}
+
+}  // namespace
+
+GemmPlan plan_gemm(const GemmRequest& rq) {
+  // 128x128 wave tiles (4 waves) win where the copies are direct and the
+  // fragments are read as vectors: 0.852 against 0.876 ms for 8 waves of
+  // 128x64 on the 8192^3 bf16 GEMM, reading 1/3 less LDS per MFMA.  Otherwise
+  // two waves per SIMD do better (register-staged 4096^3 Morton-A GEMM: 913-922
+  // TFLOP/s with 8 waves, 850 with 4; transposing fragment reads: ~3%).
+  GemmPlan p = plan_gemm_waves(rq, true);
+  if (rq.wn || p.direct_vec) return p;
+  return plan_gemm_waves(rq, false);
 }
 
 namespace {

@@ -22,7 +22,9 @@ struct GemmRequest {
   LayoutP frag_a, frag_b, frag_c;        // null: chosen; else they select the MFMA instruction
 };
 
-struct GemmPlan : KernelPlan {};
+struct GemmPlan : KernelPlan {
+  bool direct_vec = false;  // direct copies, both operands' fragments read as vectors
+};
 
 GemmRequest gemm_request(const lego_gemm_desc& d, const std::function<LayoutP(lego_layout_t)>& resolve);
 std::shared_ptr<GemmPlan> gemm_plan_cached(const GemmRequest& rq);

@@ -106,10 +106,29 @@ LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
   do {              \
   } while (0)
 #endif
+// Fragment register sets: FRAG_DIST + 1, or one per substep when that does
+// not divide the substeps of a step (a set's index must repeat every step).
+#ifndef FRAG_DIST
+#define FRAG_DIST 1
+#endif
+#if (BK / KB) % (FRAG_DIST + 1) == 0
+#define NFB (FRAG_DIST + 1)
+#else
+#define NFB (BK / KB)
+#endif
+// The reads of substep s + FRAG_DIST must go to another set than substep s
+// uses: FRAG_DIST + 1 sets at least, which needs more substeps than
+// FRAG_DIST.
+static_assert(FRAG_DIST == 1 || (FRAG_DIST < BK / KB && NFB > FRAG_DIST), "fragment sets");
 // LDS read instructions per fragment.
 #define A_FRD (A_FRTR ? 2 : (A_FRVEC ? 1 : 8))
 #define B_FRD (B_FRTR ? 2 : (B_FRVEC ? 1 : 8))
 #define FRAG_READS (MI * A_FRD + NI * B_FRD)
+
+template <bool B>
+struct lego_bool {
+  static constexpr bool value = B;
+};
 
 extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restrict__ A, const elem_t* __restrict__ B,
                                                            float* __restrict__ C) {
@@ -237,7 +256,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 
   // Fragments of one k-substep, double-buffered in registers: the reads of
   // substep s+1 are in flight while the MFMAs of substep s run.
-  mf_t af[2][MI], bf[2][NI];
+  mf_t af[NFB][MI], bf[NFB][NI];
   auto fload = [&](const elem_t* la, const elem_t* lb, int s, int buf) {
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
@@ -378,56 +397,82 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     if ((IDX_T)p < KT) dload(p, p);
   wait_tiles((int)(KT - 1 < (IDX_T)(NSTAGES - 1) ? KT - 1 : (IDX_T)(NSTAGES - 1)));
   __syncthreads();
-  fload(lds, lds + A_STAGE, 0, 0);
-  for (IDX_T kt = 0; kt < KT; ++kt) {
+  // Fragments are read FRAG_DIST substeps ahead of their MFMAs; the barrier
+  // that hands over the LDS stages sits FRAG_DIST substeps before the end of
+  // a step, so reads of the next stage can start there.
+#pragma unroll
+  for (int p = 0; p < FRAG_DIST; ++p) fload(lds, lds + A_STAGE, p, p % NFB);
+  // One K step.  MORE (a compile-time flag): tile kt+NSTAGES exists.  The
+  // loop is peeled into steps with and without it so that the body of each
+  // has no branch: a branch would keep the scheduler from placing the copies
+  // and the fragment reads between the MFMAs.
+  auto kstep = [&](IDX_T kt, auto more) {
+    constexpr bool MORE = decltype(more)::value;
+    constexpr int S = BK / KB;
     const int cur = kt % NSTAGES;
     const elem_t* la = lds + cur * STAGE;
     const elem_t* lb = la + A_STAGE;
+    const elem_t* na = lds + ((kt + 1) % NSTAGES) * STAGE;
 #pragma unroll
-    for (int s = 0; s < BK / KB; ++s) {
+    for (int s = 0; s < S; ++s) {
       FRAG_WAIT();
-      if (s == BK / KB - 1) {
-        // Every read of this stage has been issued and has completed (the
+      if (s == S - FRAG_DIST) {
+        // Every read of stage `cur` has been issued and has completed (the
         // barrier waits for this wave's LDS reads).  Once tile kt+1 has landed
         // (tiles requested after it may stay in flight) and all waves are
-        // here, stage `cur` is free for tile kt+NSTAGES, and the first
-        // fragments of step kt+1 are fetched while the MFMAs of this last
-        // substep run.
-        const IDX_T last = (kt + NSTAGES - 1 < KT ? kt + NSTAGES - 1 : KT - 1);
-        wait_tiles(last > kt + 1 ? (int)(last - (kt + 1)) : 0);
+        // here, stage `cur` is free for tile kt+NSTAGES and the fragments of
+        // step kt+1 can be read.
+        if constexpr (MORE) {
+          wait_tiles(NSTAGES - 2);
+        } else {
+          const IDX_T last = KT - 1;
+          wait_tiles(last > kt + 1 ? (int)(last - (kt + 1)) : 0);
+        }
+        // This wave's reads of stage `cur` must be complete before any wave
+        // copies into it (the barrier alone does not wait for LDS reads).
+        __builtin_amdgcn_s_waitcnt(0xC07F);
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
       }
+      // Reads for substep t of this step, or of the next one past the end
+      // (after the last step those read a stage that is never used again: in
+      // bounds, and waited for below).
+      const int t = s + FRAG_DIST;
+      const elem_t* ra = t < S ? la : na;
+      const int ts = t < S ? t : t - S;
 #if DMA_SPREAD
-      if (s == BK / KB - 1) {
+      if (s >= S - FRAG_DIST) {
         // The copies of tile kt+NSTAGES go out between the rows of MFMAs, a
         // share after each row, so the matrix pipe is never left idle while
-        // the wave issues a burst of them.
+        // the wave issues a burst of them; the fragment reads go out after
+        // the first row, and the remaining rows cover their latency.
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
 #pragma unroll
-          for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+          for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s % NFB][i], bf[s % NFB][j], acc[i][j]);
           __builtin_amdgcn_sched_barrier(0);
-          if (kt + NSTAGES < KT) dload_part(kt + NSTAGES, cur, i * (A_NV + B_NV) / MI, (i + 1) * (A_NV + B_NV) / MI);
+          constexpr int R = FRAG_DIST * MI;
+          const int r = (s - (S - FRAG_DIST)) * MI + i;
+          if constexpr (MORE) dload_part(kt + NSTAGES, cur, r * (A_NV + B_NV) / R, (r + 1) * (A_NV + B_NV) / R);
+          if (i == 0) fload(ra, ra + A_STAGE, ts, ts % NFB);
           __builtin_amdgcn_sched_barrier(0);
         }
-      } else
+        continue;
+      }
 #else
-      if (s == BK / KB - 1 && kt + NSTAGES < KT) dload(kt + NSTAGES, cur);
+      if constexpr (MORE) {
+        if (s == S - FRAG_DIST) dload(kt + NSTAGES, cur);
+      }
 #endif
 #pragma unroll
       for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
-      // Fragments of the next substep are read between these MFMAs, never
-      // ahead of them: with direct loads in flight the only wait the compiler
-      // can place before an MFMA is one for every outstanding LDS read, so a
-      // read issued before this block would stall it.
-      if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
-      else if (kt + 1 < KT) {
-        const elem_t* na = lds + ((kt + 1) % NSTAGES) * STAGE;
-        fload(na, na + A_STAGE, 0, 0);
-      }
+        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s % NFB][i], bf[s % NFB][j], acc[i][j]);
+      // The reads are placed between these MFMAs, never ahead of them: with
+      // direct loads in flight the only wait the compiler can place before an
+      // MFMA is one for every outstanding LDS read, so a read issued before
+      // this block would stall it.
+      fload(ra, ra + A_STAGE, ts, ts % NFB);
 #pragma unroll
       for (int g = 0; g < (FRAG_READS < MI * NI ? FRAG_READS : MI * NI); ++g) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
@@ -437,7 +482,14 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       __builtin_amdgcn_sched_group_barrier(0x100, FRAG_READS, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-  }
+  };
+  IDX_T kt = 0;
+  for (; kt + NSTAGES < KT; ++kt) kstep(kt, lego_bool<true>{});
+  for (; kt < KT; ++kt) kstep(kt, lego_bool<false>{});
+  // The reads issued in the last step are dead; let them land before the
+  // registers they target are reused.
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_sched_barrier(0);
 #elif (PREFETCH == 2 || ROLLING) && BK / KB >= 2
   // Register-staged pipeline.  With one wave per SIMD (the accumulators
   // fill the AGPRs) no other wave hides a stall, and with two the loads and

@@ -158,7 +158,8 @@ def test_plans_choose_expected_paths(lego):
     p = L.remap_plan(L.as_layout(L.Row(6, 6)), L.as_layout(L.GenP("antidiag", [6, 6])), 4)
     assert p["path"] == "gather"
     info = L.gemm_plan(8192, 8192, 8192, "bf16")
-    assert "direct-lds" in info and "A:V8k sep" in info and "frvec" in info
+    assert "direct-lds spread fd2" in info and "A:V8k sep" in info and "frvec" in info
+    assert "waves 2x2 wave 128x128" in info
 
 
 def test_binding_checks_buffer_sizes_before_launch(lego):

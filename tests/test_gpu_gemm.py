@@ -107,22 +107,25 @@ def test_gemm_fragment_layouts_select_the_instruction(lego, instr):
     assert ok, (mre, fre)
 
 
-@pytest.mark.parametrize("staged", [False, True])
-def test_gemm_one_wave_per_simd(lego, staged):
-    """128x128 wave tiles (256 accumulators, one wave per SIMD): the direct
-    copies spread over the last substep, and, with A in 2x4 blocks, the
-    register-staged rolling pipeline; 1024x512x1024 bf16 against the oracle."""
+@pytest.mark.parametrize("staged,wn", [(False, 128), (True, 128), (False, 64), (True, 64)])
+def test_gemm_wave_tiles(lego, staged, wn):
+    """256x256 workgroup tiles with 128x128 wave tiles (256 accumulators, one
+    wave per SIMD, the default) and with 128x64 wave tiles (two waves per
+    SIMD): direct copies spread over the last substep with fragments read two
+    substeps ahead, and, with A in 2x4 blocks, the register-staged rolling
+    pipeline; 1024x512x1024 bf16 against the oracle."""
     M, N, K = 1024, 512, 1024
     a = S.tensor(M * K, "bf16", dist="normal", seed=S.SEED_A)
     b = S.tensor(K * N, "bf16", dist="normal", seed=S.SEED_B)
-    kw = dict(bm=256, bn=256, bk=64, wm=128, wn=128)
+    kw = dict(bm=256, bn=256, bk=64, wm=128, wn=wn)
     ola = OL.as_layout(OL.Row(M, K))
     if staged:
         kw["a"] = lego.TileOrderBy(lego.Row(M // 2, K // 4), lego.Row(2, 4))
         ola = OL.TileOrderBy(OL.Row(M // 2, K // 4), OL.Row(2, 4))
     plan = lego.gemm_plan(M, N, K, "bf16", **kw)
-    say(f"gemm one wave per SIMD staged={staged} plan={plan}")
-    assert ("staged" in plan) == staged and "wave 128x128" in plan
+    say(f"gemm wave tiles 128x{wn} staged={staged} plan={plan}")
+    assert ("staged" in plan) == staged and f"wave 128x{wn}" in plan
+    assert staged or "spread fd2" in plan
     c = _run(lego, a, b, M, N, K, "bf16", **kw).reshape(M, N)
     r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), ola, OL.as_layout(OL.Col(K, N)), "bf16")
     ok, mre, fre = OG.check_tolerance(c, r)
