@@ -348,10 +348,16 @@ def bench_extra(L, reps=20):
     f, i = _alternate(L, row, mz, x, y, z, reps)
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     ff, fi = _flushed(L, row, mz, x, y, z, scratch, reps)
+    # The practical ceiling at this size: the identity remap (a plain vector
+    # copy of the same 64 MiB per launch), hot and flushed.
+    cf, ci = _alternate(L, row, row, x, y, z, reps)
+    cff, cfi = _flushed(L, row, row, x, y, z, scratch, reps)
     del scratch
     out["morton_f16_4096"] = {"bytes_per_launch": nb, "hot_row_to_morton_GBps": gbps(nb, f),
                               "hot_morton_to_row_GBps": gbps(nb, i), "flushed_row_to_morton_GBps": gbps(nb, ff),
                               "flushed_morton_to_row_GBps": gbps(nb, fi),
+                              "identity_copy_hot_GBps": gbps(nb, (cf + ci) / 2),
+                              "identity_copy_flushed_GBps": gbps(nb, (cff + cfi) / 2),
                               "plan": L.remap_plan(row, mz, 2)["info"]}
 
     a_log = S.tensor(n * n, "f16", seed=S.SEED_A).cuda()

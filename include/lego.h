@@ -202,8 +202,11 @@ lego_status lego_remap(lego_layout_t src, lego_layout_t dst, int elem_bytes, con
                        void* stream);
 
 /* The plan lego_remap would use: path 0 direct vector copy, 1 LDS-tiled, 2
- * element gather; run = contiguous run length of the map; vec = elements per
- * vector; tile = elements per LDS tile (0 if none).  info (may be NULL) gets a
+ * element gather, 3 box-staged (a 2-D map without digit structure, such as
+ * the antidiagonal order of Figure 7, copied through LDS one square box of
+ * the logical index space at a time, read and written in the orders under
+ * which each side is contiguous); run = contiguous run length of the map;
+ * vec = elements per vector; tile = elements per LDS tile or box (0 if none).  info (may be NULL) gets a
  * text summary of at most info_cap bytes. */
 lego_status lego_remap_plan(lego_layout_t src, lego_layout_t dst, int elem_bytes, int* path, int64_t* run,
                             int* vec, int64_t* tile, char* info, size_t info_cap);

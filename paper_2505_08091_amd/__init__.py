@@ -349,7 +349,7 @@ def remap_plan(src_layout, dst_layout, elem_bytes):
     info = ctypes.create_string_buffer(4096)
     _check(_lib.lego_remap_plan(src_layout.h, dst_layout.h, int(elem_bytes), ctypes.byref(path), ctypes.byref(run),
                                 ctypes.byref(vec), ctypes.byref(tile), info, 4096))
-    return {"path": ("direct", "lds", "gather")[path.value], "run": run.value, "vec": vec.value,
+    return {"path": ("direct", "lds", "gather", "box")[path.value], "run": run.value, "vec": vec.value,
             "tile": tile.value, "info": info.value.decode()}
 
 

@@ -501,20 +501,40 @@ bool digits_of(const Ctx& c, const Sum& s, int v, std::vector<Digit>* out) {
 // ------------------------------------------------------------------ print --
 namespace {
 
+// 32-bit index code computes sums, products and selects modulo 2^32, which
+// gives the true value wherever that value lies in [0, 2^32) whatever the
+// intermediate values were; the other operations (floor division, modulo,
+// comparison, xor, square root, a select's condition) need their operands'
+// true values, so those must be proven in [0, 2^32) by their ranges.
 bool sum_fits32(const Sum& s);
 
-bool atom_fits32(const Atom& a) {
-  for (auto& k : a.kids)
-    if (!sum_fits32(k)) return false;
-  return a.r.lo >= 0 && a.r.hi < (i64(1) << 32);
+// The 32-bit evaluation of `s` is congruent to its value modulo 2^32.
+bool sum_ring32(const Sum& s);
+
+bool atom_ring32(const Atom& a) {
+  switch (a.op) {
+    case Op::Mul:
+      return sum_ring32(a.kids[0]) && sum_ring32(a.kids[1]);
+    case Op::Select:
+      return sum_fits32(a.kids[0]) && sum_ring32(a.kids[1]) && sum_ring32(a.kids[2]);
+    default:
+      for (auto& k : a.kids)
+        if (!sum_fits32(k)) return false;
+      return a.r.lo >= 0 && a.r.hi < (i64(1) << 32);
+  }
 }
 
+bool sum_ring32(const Sum& s) {
+  for (auto& t : s.t)
+    if (!atom_ring32(*t.a)) return false;
+  return true;
+}
+
+// The 32-bit evaluation of `s` is its value.
 bool sum_fits32(const Sum& s) {
   Interval r = range(s);
   if (r.lo < 0 || r.hi >= (i64(1) << 32)) return false;
-  for (auto& t : s.t)
-    if (!atom_fits32(*t.a)) return false;
-  return true;
+  return sum_ring32(s);
 }
 
 struct Printer {
@@ -638,6 +658,7 @@ struct Printer {
 }  // namespace
 
 bool fits32(const Sum& s) { return sum_fits32(s); }
+bool ring32(const Sum& s) { return sum_ring32(s); }
 
 Printed print(const Ctx& c, const Sum& s) {
   PrintedMany m = print_many(c, {s}, !sum_fits32(s));

@@ -126,6 +126,9 @@ struct PrintedMany {
   int ops = 0;
 };
 PrintedMany print_many(const Ctx& c, const std::vector<Sum>& outs, bool wide);
+// 32-bit index code evaluates s exactly (fits32), or congruently modulo 2^32
+// (ring32: exact wherever the value is known to lie in [0, 2^32)).
 bool fits32(const Sum& s);
+bool ring32(const Sum& s);
 
 }  // namespace lego

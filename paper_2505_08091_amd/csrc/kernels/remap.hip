@@ -18,6 +18,13 @@
 //   LEGO_FN IDX_T ldsw(IDX_T q, IDX_T e)      LDS slot of element e of that vector
 //   LEGO_FN IDX_T ldsr(IDX_T q)               LDS slot of destination-side vector q
 //   LEGO_FN IDX_T dst_off(IDX_T g, IDX_T q)   element offset of destination-side vector q
+// Box path (2-D maps without digit structure): a BR x BC box of the logical
+// index space is read in one order and written in another, through LDS:
+//   BR, BC, BPAD, NBC (boxes per row of boxes), EXT0, EXT1 (logical extents), NT
+//   LEGO_FN void ws(IDX_T q, IDX_T* a, IDX_T* b)   box element read q-th
+//   LEGO_FN void wd(IDX_T q, IDX_T* a, IDX_T* b)   box element written q-th
+//   LEGO_FN IDX_T bsrc(IDX_T i, IDX_T j), bdst(IDX_T i, IDX_T j)   element
+//                                    offsets of logical point (i, j)
 // NONTEMPORAL: bit 0 streams (non-temporal) global loads, bit 1 stores.
 
 #if NONTEMPORAL & 1
@@ -123,4 +130,40 @@ extern "C" __global__ __launch_bounds__(NT) void lego_remap_lds(const ELEM_T* __
     LEGO_ST(w, (vs_t*)(dst + dst_off(g, q)));
   }
 }
+#endif
+
+#ifdef LEGO_REMAP_BOX
+// One workgroup per box.  The read order makes consecutive lanes read
+// consecutive source addresses, the write order consecutive destination
+// addresses (runs of up to a box side); each LDS row is BC + BPAD elements,
+// the pad chosen so that neither order puts two lanes of a wave on one bank.
+// Points past the logical extents (boxes on the last row or column) are
+// neither read nor written.
+#define BOX (BR * BC)
+extern "C" __global__ __launch_bounds__(NT) void lego_remap_box(const ELEM_T* __restrict__ src,
+                                                                ELEM_T* __restrict__ dst) {
+  __shared__ ELEM_T tile[BR * (BC + BPAD)];
+  const IDX_T i0 = (IDX_T)(blockIdx.x / NBC) * BR, j0 = (IDX_T)(blockIdx.x % NBC) * BC;
+  const bool whole = i0 + BR <= EXT0 && j0 + BC <= EXT1;
+  ELEM_T v[BOX / NT];
+  IDX_T slot[BOX / NT];
+  // All reads first, so that BOX / NT loads per thread are in flight at once.
+#pragma unroll
+  for (int u = 0; u < BOX / NT; ++u) {
+    IDX_T a, b;
+    ws((IDX_T)(u * NT + threadIdx.x), &a, &b);
+    slot[u] = a * (BC + BPAD) + b;
+    if (whole || (i0 + a < EXT0 && j0 + b < EXT1)) v[u] = LEGO_LD(src + bsrc(i0 + a, j0 + b));
+  }
+#pragma unroll
+  for (int u = 0; u < BOX / NT; ++u) tile[slot[u]] = v[u];
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < BOX / NT; ++u) {
+    IDX_T a, b;
+    wd((IDX_T)(u * NT + threadIdx.x), &a, &b);
+    if (whole || (i0 + a < EXT0 && j0 + b < EXT1)) LEGO_ST(tile[a * (BC + BPAD) + b], dst + bdst(i0 + a, j0 + b));
+  }
+}
+#undef BOX
 #endif

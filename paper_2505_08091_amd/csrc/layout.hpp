@@ -320,15 +320,18 @@ std::vector<typename A::V> Piece::genp_inv(const A& al, const typename A::V& x) 
       return out;
     }
     case GEN_ANTIDIAG: {
-      // Figure 7 inverse with the exact integer square root.
+      // Figure 7 inverse with the exact integer square root.  In the upper
+      // triangle y = d(d+1)/2 + i with 0 <= i <= d on antidiagonal d, so
+      // (2d+1)^2 <= 8y+1 < (2d+3)^2 and d = (isqrt(8y+1) - 1) / 2 exactly;
+      // the lower triangle is the upper one turned by 180 degrees.  (Every
+      // intermediate is non-negative, so 32-bit index code can evaluate it.)
       i64 nn = n[0];
       i64 S = nn * (nn + 1) / 2;
       V upper = al.lt(x, al.c(S));
       V y = al.sel(upper, x, al.sub(al.c(nn * nn - 1), x));
-      V a = al.isqrt(al.mulc(y, 2));
-      a = al.add(a, al.sub(al.c(1), al.lt(y, al.div(al.mul(a, al.add(a, al.c(1))), 2))));
-      V i = al.sub(y, al.div(al.mul(a, al.sub(a, al.c(1))), 2));
-      V j = al.sub(al.sub(a, i), al.c(1));
+      V d = al.div(al.sub(al.isqrt(al.add(al.mulc(y, 8), al.c(1))), al.c(1)), 2);
+      V i = al.sub(y, al.div(al.mul(d, al.add(d, al.c(1))), 2));
+      V j = al.sub(d, i);
       return {al.sel(upper, i, al.sub(al.c(nn - 1), i)), al.sel(upper, j, al.sub(al.c(nn - 1), j))};
     }
   }

@@ -9,7 +9,10 @@ namespace lego {
 std::string fn_text(const Ctx& c, const std::string& name, const FnSpec& f, bool force_wide, int* ops,
                     bool* wide) {
   bool w = force_wide;
-  for (auto& o : f.outs) w = w || !fits32(o);
+  for (size_t k = 0; k < f.outs.size(); ++k) {
+    const bool bounded = k < f.out_bound.size() && f.out_bound[k] > 0 && f.out_bound[k] <= (i64(1) << 32);
+    w = w || !(bounded ? ring32(f.outs[k]) : fits32(f.outs[k]));
+  }
   for (int v : f.params) w = w || c.vars[v].hi >= (i64(1) << 32);
   const char* T = w ? "i64" : "u32";
   std::ostringstream s;
@@ -79,6 +82,8 @@ FnSpec spec_apply_flat(Ctx& c, const Layout& l) {
   FnSpec f;
   f.params = {x};
   f.outs = {l.apply(al, idx)};
+  // a bijection onto [0, phys_size) (ExpandBy's apply is -1 off its extents)
+  if (!l.expand_inner) f.out_bound = {l.phys_size()};
   return f;
 }
 
@@ -88,6 +93,7 @@ FnSpec spec_inv_flat(Ctx& c, const Layout& l) {
   FnSpec f;
   f.params = {p};
   f.outs = l.inv(al, var(c, p));
+  if (!l.expand_inner) f.out_bound = l.dims();
   return f;
 }
 
@@ -133,7 +139,15 @@ LEGO_FN u64 lego_isqrt_u64(u64 v) {
   }
   return r;
 }
-LEGO_FN u32 lego_isqrt(u32 v) { return (u32)lego_isqrt_u64(v); }
+// 32-bit operands: the square root of the nearest float, corrected to the
+// exact floor by integer comparisons (the estimate is off by at most one for
+// every 32-bit v; the loops make the result exact whatever the estimate).
+LEGO_FN u32 lego_isqrt(u32 v) {
+  u64 r = (u64)__builtin_sqrtf((float)v);
+  while (r * r > v) --r;
+  while ((r + 1) * (r + 1) <= v) ++r;
+  return (u32)r;
+}
 LEGO_FN i64 lego_isqrt(i64 v) { return v <= 0 ? 0 : (i64)lego_isqrt_u64((u64)v); }
 )PRELUDE";
 }

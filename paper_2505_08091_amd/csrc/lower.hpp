@@ -21,6 +21,10 @@ struct FnSpec {
   std::vector<Sum> outs;    // one or more outputs
   bool out_array = false;   // write outputs to one array parameter `o`
   bool valid = true;        // false: this variant cannot express the function
+  // Optional: output k is known to lie in [0, out_bound[k]) (a layout's
+  // inverse within its extents, its forward map within its physical size),
+  // which lets 32-bit code compute it through out-of-range intermediates.
+  std::vector<i64> out_bound;
 };
 
 struct Emitted {

@@ -40,7 +40,7 @@ struct KernelPlan {
 // which = 1 inv (physical order, `rank` outputs per point).
 KernelPlan plan_index_eval(const Layout& l, int which, int idx_bytes);
 
-enum RemapPath { REMAP_DIRECT = 0, REMAP_LDS = 1, REMAP_GATHER = 2 };
+enum RemapPath { REMAP_DIRECT = 0, REMAP_LDS = 1, REMAP_GATHER = 2, REMAP_BOX = 3 };
 
 struct RemapPlan : KernelPlan {
   int path = REMAP_GATHER;

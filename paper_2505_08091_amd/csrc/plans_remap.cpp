@@ -182,6 +182,117 @@ RemapPlan plan_remap(const Layout& src, const Layout& dst, int elem_bytes) {
   }
 }
 
+// Box-staged remap for 2-D maps without digit structure (an element gather
+// otherwise; e.g. Row <-> antidiagonal order).  A B x B box of the logical
+// index space goes through LDS: its elements are read in the order ws (a
+// layout over the box) under which the source layout is most contiguous, and
+// written in the order wd under which the destination layout is.  The orders
+// are chosen among Row, Col and the antidiagonal GenP of the box by counting,
+// on the host, the breaks in the address sequence over a sample box.  Returns
+// false when no order gives runs of 8 elements on average on both sides.
+static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes, RemapPlan* out) {
+  const std::vector<i64> n = src.dims();
+  if (n.size() != 2) return false;
+  const i64 B = elem_bytes <= 4 ? 64 : 32;
+  if (n[0] < B || n[1] < B) return false;
+  const std::vector<std::pair<std::string, LayoutP>> orders = {
+      {"row", make_from_piece(make_row({B, B}))},
+      {"col", make_from_piece(make_col({B, B}))},
+      {"antidiag", make_from_piece(make_genp(GEN_ANTIDIAG, {B, B}, {}))}};
+  // A box away from the edges when there is one (the first otherwise).
+  const i64 o0 = n[0] >= 3 * B ? B : 0, o1 = n[1] >= 3 * B ? B : 0;
+  auto breaks = [&](const Layout& L, const Layout& W) {
+    i64 prev = 0, nb = 0;
+    for (i64 q = 0; q < B * B; ++q) {
+      const std::vector<i64> ab = host_inv(W, q);
+      const i64 x = host_apply(L, {o0 + ab[0], o1 + ab[1]});
+      if (q == 0 || x != prev + 1) ++nb;
+      prev = x;
+    }
+    return nb;
+  };
+  size_t ws = 0, wd = 0;
+  i64 bs = -1, bd = -1;
+  for (size_t k = 0; k < orders.size(); ++k) {
+    const i64 x = breaks(src, *orders[k].second), y = breaks(dst, *orders[k].second);
+    if (bs < 0 || x < bs) bs = x, ws = k;
+    if (bd < 0 || y < bd) bd = y, wd = k;
+  }
+  if (bs * 8 > B * B || bd * 8 > B * B) return false;
+  // LDS slot of box element (a, b): a * (B + pad) + b, with the pad that
+  // keeps the 64 lanes of a wave on distinct 4-byte banks under both orders
+  // (Row/antidiagonal: 0, strides 1 and B-1; Col needs a pad).
+  int pad = 0;
+  {
+    int best = 1 << 30;
+    for (int pd = 0; pd < 4; ++pd) {
+      int cost = 0;
+      for (size_t k : {ws, wd})
+        for (i64 q0 : {i64(0), B * B / 2}) {
+          std::vector<int> hits(64, 0);
+          int worst = 0;
+          for (i64 l = 0; l < 64; ++l) {
+            const std::vector<i64> ab = host_inv(*orders[k].second, q0 + l);
+            const i64 slot = ab[0] * (B + pd) + ab[1];
+            worst = std::max(worst, ++hits[(slot * elem_bytes / 4) % 64]);
+          }
+          cost += worst;
+        }
+      if (cost < best) best = cost, pad = pd;
+    }
+  }
+  const int NT = 256;
+  const i64 nbr = (n[0] + B - 1) / B, nbc = (n[1] + B - 1) / B;
+  const LayoutP Ws = orders[ws].second, Wd = orders[wd].second;
+  auto order_fn = [&](const LayoutP& W) {
+    return [&, W](Ctx& c) {
+      int q = c.var("q", B * B);
+      SymAlg al{&c};
+      FnSpec f;
+      f.params = {q};
+      f.outs = W->inv(al, var(c, q));
+      f.out_bound = {B, B};
+      return f;
+    };
+  };
+  auto addr_fn = [&](const Layout* L) {
+    return [&, L](Ctx& c) {
+      int i = c.var("i", n[0]), j = c.var("j", n[1]);
+      SymAlg al{&c};
+      FnSpec f;
+      f.params = {i, j};
+      f.outs = {L->apply(al, {var(c, i), var(c, j)})};
+      f.out_bound = {L->phys_size()};
+      return f;
+    };
+  };
+  std::string info;
+  bool wide = false;
+  std::string fns = emit_all({{"ws", order_fn(Ws)}, {"wd", order_fn(Wd)}, {"bsrc", addr_fn(&src)}, {"bdst", addr_fn(&dst)}},
+                             &wide, &info);
+  int nontemporal = 0;
+  if (const char* e = std::getenv("LEGO_REMAP_NONTEMPORAL")) nontemporal = std::atoi(e);
+  std::ostringstream s;
+  s << header() << "#define ELEM_T " << elem_type(elem_bytes) << "\n#define IDX_T " << (wide ? "i64" : "u32")
+    << "\n#define BR " << B << "\n#define BC " << B << "\n#define BPAD " << pad << "\n#define NBC " << nbc
+    << "\n#define EXT0 " << n[0] << "\n#define EXT1 " << n[1] << "\n#define NT " << NT
+    << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_BOX 1\n"
+    << fns << "// ---- template ----\n" << tpl_remap;
+  RemapPlan& R = *out;
+  R.path = REMAP_BOX;
+  R.run = 1;
+  R.vec = R.vec_dst = 1;
+  R.tile = B * B;
+  R.kernel = "lego_remap_box";
+  R.block = NT;
+  R.grid = nbr * nbc;
+  R.src = s.str();
+  R.info = "box " + std::to_string(B) + "x" + std::to_string(B) + " load " + orders[ws].first + " (" +
+           std::to_string(bs) + " runs) store " + orders[wd].first + " (" + std::to_string(bd) + " runs) pad " +
+           std::to_string(pad) + " NT=" + std::to_string(NT) + info;
+  return true;
+}
+
 static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_bytes, bool allow_lds) {
   const char* et = elem_type(elem_bytes);
   if (src.dims() != dst.dims()) throw std::length_error("remap layouts have different logical shapes");
@@ -240,6 +351,13 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     R.path = REMAP_LDS;
   } else {
     R.path = V > 1 ? REMAP_DIRECT : REMAP_GATHER;
+  }
+
+  if (R.path == REMAP_GATHER && !masked && !dst.expand_inner && N == NS) {
+    RemapPlan box;
+    bool use = plan_remap_box(src, dst, elem_bytes, &box);
+    if (const char* e = std::getenv("LEGO_REMAP_BOX")) use = use && std::atoi(e) != 0;
+    if (use) return box;
   }
 
   std::ostringstream s;

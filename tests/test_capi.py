@@ -157,6 +157,12 @@ def test_plans_choose_expected_paths(lego):
     assert p["path"] == "lds" and p["vec"] == 8
     p = L.remap_plan(L.as_layout(L.Row(6, 6)), L.as_layout(L.GenP("antidiag", [6, 6])), 4)
     assert p["path"] == "gather"
+    n = 4096
+    row, ad = L.as_layout(L.Row(n, n)), L.as_layout(L.GenP("antidiag", [n, n]))
+    p = L.remap_plan(row, ad, 4)
+    assert p["path"] == "box" and p["tile"] == 4096 and "load row (64 runs) store antidiag (127 runs)" in p["info"]
+    p = L.remap_plan(ad, row, 4)
+    assert p["path"] == "box" and "load antidiag (127 runs) store row (64 runs)" in p["info"]
     info = L.gemm_plan(8192, 8192, 8192, "bf16")
     assert "direct-lds spread fd2" in info and "A:V8k sep" in info and "frvec" in info
     assert "waves 2x2 wave 128x128" in info

@@ -70,6 +70,42 @@ int main(int argc, char** argv) {
     if ((s + 1) * V > nsrc) FAIL("src_vec(%llu) = %llu out of range", (unsigned long long)t, (unsigned long long)s);
     for (int e = 0; e < V; ++e) perm[t * V + e] = (long long)(s * V + e);
   }
+#elif defined(LEGO_REMAP_BOX)
+  const u64 n = (u64)EXT0 * EXT1, nsrc = n;
+  if ((BR * BC) % NT || NT > 256) FAIL("NT does not divide the box");
+  if ((unsigned long long)BR * (BC + BPAD) * sizeof(ELEM_T) > 65536) FAIL("box exceeds 64 KiB of LDS");
+  const u64 nbr = (EXT0 + BR - 1) / BR;
+  std::vector<long long> perm(n, -2);
+  std::vector<long long> tile((u64)BR * (BC + BPAD));
+  for (u64 bx = 0; bx < nbr * NBC; ++bx) {
+    const u64 i0 = (bx / NBC) * BR, j0 = (bx % NBC) * BC;
+    std::fill(tile.begin(), tile.end(), -1);
+    std::vector<char> rseen(BR * BC), wseen(BR * BC);
+    for (u64 q = 0; q < (u64)BR * BC; ++q) {
+      IDX_T a, b;
+      ws((IDX_T)q, &a, &b);
+      if (a >= BR || b >= BC) FAIL("ws(%llu) outside the box", (unsigned long long)q);
+      if (rseen[a * BC + b]++) FAIL("ws is not a bijection onto the box");
+      if (i0 + a < EXT0 && j0 + b < EXT1) {
+        u64 s = (u64)bsrc((IDX_T)(i0 + a), (IDX_T)(j0 + b));
+        if (s >= nsrc) FAIL("bsrc out of range");
+        tile[a * (BC + BPAD) + b] = (long long)s;
+      }
+    }
+    for (u64 q = 0; q < (u64)BR * BC; ++q) {
+      IDX_T a, b;
+      wd((IDX_T)q, &a, &b);
+      if (a >= BR || b >= BC) FAIL("wd(%llu) outside the box", (unsigned long long)q);
+      if (wseen[a * BC + b]++) FAIL("wd is not a bijection onto the box");
+      if (i0 + a < EXT0 && j0 + b < EXT1) {
+        u64 d = (u64)bdst((IDX_T)(i0 + a), (IDX_T)(j0 + b));
+        if (d >= n) FAIL("bdst out of range");
+        if (perm[d] != -2) FAIL("destination written twice");
+        if (tile[a * (BC + BPAD) + b] < 0) FAIL("LDS slot read before written");
+        perm[d] = tile[a * (BC + BPAD) + b];
+      }
+    }
+  }
 #else
   const u64 n = NELEM, nsrc = NELEM;
   if (NT < 1 || NT > 256 || (TILE / VL) % NT || (TILE / VS) % NT) FAIL("NT does not divide the tile's vectors");
@@ -485,3 +521,48 @@ def test_gemm_sources_of_gpu_cases(i):
     src = L.plan_source("gemm", **kw)
     with tempfile.TemporaryDirectory() as tmp:
         assert _compile_and_run(src, HARNESS_GEMM, tmp).strip() == "ok", kw
+
+
+HARNESS_ISQRT = r"""
+int main() {
+  // 32-bit: every v below 2^20, and k^2 - 1, k^2, k^2 + 1 for every k < 2^16
+  // (where a float estimate could round across the boundary), and the top.
+  unsigned long long bad = 0;
+  auto ok32 = [&](u64 v) {
+    const u64 r = lego_isqrt((u32)v);
+    if (!(r * r <= v && (r + 1) * (r + 1) > v)) ++bad;
+  };
+  for (u64 v = 0; v < (1ull << 20); ++v) ok32(v);
+  for (u64 k = 1; k < (1ull << 16); ++k) { ok32(k * k - 1); ok32(k * k); if (k * k + 1 < (1ull << 32)) ok32(k * k + 1); }
+  for (u64 v = 0xFFFFFFFFull - 4096; v <= 0xFFFFFFFFull; ++v) ok32(v);
+  // 64-bit: values from the command line, one per line of stdin
+  unsigned long long x;
+  while (scanf("%llu", &x) == 1) printf("%lld\n", (long long)lego_isqrt((i64)x));
+  fprintf(stderr, "bad32 %llu\n", bad);
+  return bad != 0;
+}
+"""
+
+
+def test_integer_square_root_of_generated_code():
+    """The exact integer square root the kernels use (the antidiagonal GenP,
+    Figure 7 with an exact root): 32-bit operands at every perfect-square
+    boundary, 64-bit ones against math.isqrt on sampled values."""
+    import math
+    import random
+    import paper_2505_08091_amd as L
+    src = L.plan_source("apply", L.as_layout(L.GenP("antidiag", [64, 64])), param=4)
+    rng = random.Random(5)
+    vals = [0, 1, 2, 3, (1 << 62) - 1, 1 << 62, (1 << 63) - 1] + [rng.randrange(1 << 63) for _ in range(2000)]
+    vals += [k * k + d for k in (rng.randrange(1 << 31) for _ in range(500)) for d in (-1, 0, 1)]
+    with tempfile.TemporaryDirectory() as tmp:
+        head = src.split(MARK)[0]
+        cpp, exe = os.path.join(tmp, "s.cpp"), os.path.join(tmp, "s")
+        with open(cpp, "w") as f:
+            f.write(HARNESS_COMMON + head + HARNESS_ISQRT)
+        r = subprocess.run(["g++", "-O2", "-std=c++17", "-w", cpp, "-o", exe], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr[-4000:]
+        r = subprocess.run([exe], input="\n".join(map(str, vals)), capture_output=True, text=True, timeout=120)
+        assert r.returncode == 0, r.stderr
+        got = [int(t) for t in r.stdout.split()]
+        assert got == [math.isqrt(v) for v in vals]

@@ -151,10 +151,18 @@ def _small_cases(L):
          OL.as_layout(OL.Row(200, 1000)), OL.as_layout(OL.Col(200, 1000))),
         ("transpose 192x320", L.as_layout(L.Row(192, 320)), L.as_layout(L.Col(192, 320)),
          OL.as_layout(OL.Row(192, 320)), OL.as_layout(OL.Col(192, 320))),
-        # a whole matrix in antidiagonal order (Figure 7's GenP): the element
-        # gather with cached loads and per-XCD chunk ranges
+        # a whole matrix in antidiagonal order (Figure 7's GenP): 64x64 boxes
+        # read in row order and written in antidiagonal order (or the
+        # reverse), with ragged last boxes at 1000 and 130; at 63 the element
+        # gather
         ("antidiagonal 1024^2", L.as_layout(L.Row(1024, 1024)), L.as_layout(L.GenP("antidiag", [1024, 1024])),
          OL.as_layout(OL.Row(1024, 1024)), OL.as_layout(OL.antidiag_genp(1024))),
+        ("antidiagonal 1000^2", L.as_layout(L.Row(1000, 1000)), L.as_layout(L.GenP("antidiag", [1000, 1000])),
+         OL.as_layout(OL.Row(1000, 1000)), OL.as_layout(OL.antidiag_genp(1000))),
+        ("antidiagonal 130^2", L.as_layout(L.Row(130, 130)), L.as_layout(L.GenP("antidiag", [130, 130])),
+         OL.as_layout(OL.Row(130, 130)), OL.as_layout(OL.antidiag_genp(130))),
+        ("antidiagonal 63^2 (gather)", L.as_layout(L.Row(63, 63)), L.as_layout(L.GenP("antidiag", [63, 63])),
+         OL.as_layout(OL.Row(63, 63)), OL.as_layout(OL.antidiag_genp(63))),
         # 3-D bricks (the stencil data layout of Section V): small ragged bricks and 8^3 bricks
         ("3-D bricks 2x5x3 of 6x10x12", L.as_layout(L.Row(6, 10, 12)), L.TileOrderBy(L.Row(3, 2, 4), L.Row(2, 5, 3)),
          OL.as_layout(OL.Row(6, 10, 12)), OL.TileOrderBy(OL.Row(3, 2, 4), OL.Row(2, 5, 3))),
