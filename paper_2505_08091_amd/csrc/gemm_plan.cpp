@@ -744,6 +744,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
       << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "FRTR " << (o.frtr ? 1 : 0) << "\n#define " << P2[k]
       << "NVEC " << o.NVEC << "u\n#define " << P2[k]
       << "GUARD " << (o.guard ? 1 : 0) << "\n#define " << P2[k] << "EDGE " << (o.edge ? 1 : 0) << "\n#define "
+      << P2[k] << "BUF " << (o.direct && 2 * o.glob->phys_size() < (i64(1) << 31) ? 1 : 0) << "\n#define "
       << P2[k] << "BYTES " << 2 * o.glob->phys_size() << "u\n#define " << P2[k] << "VR " << o.VR << "\n#define "
       << P2[k] << "VC " << (o.axis == 2 ? o.VC : o.V) << "\n";
     // Block vectors: element index of block position (r, c), row-major.
