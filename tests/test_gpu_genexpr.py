@@ -26,6 +26,10 @@ def _wavefront(L, G, n, t):
         L.GenPExpr([q, q], GE.ANTIDIAG_APPLY, GE.ANTIDIAG_INV), L.Row(t, t))
 
 
+SKEW_APPLY = "i1 * n0 + (i0 + i1) % n0"
+SKEW_INV = ["(x % n0 + n0 - (x / n0) % n0) % n0", "x / n0"]
+
+
 def _expr_cases(L):
     return [
         ("wavefront 2048^2 of 64x64 tiles", L.as_layout(L.Row(2048, 2048)), _wavefront(L, None, 2048, 64),
@@ -36,6 +40,12 @@ def _expr_cases(L):
          OL.as_layout(OL.Row(512, 512)),
          OL.GroupBy([512, 512]).OrderBy(OL.RegP([64, 8, 64, 8], [1, 3, 2, 4])).OrderBy(
              OL.Row(64, 64), GX.expr_genp([8, 8], GE.MORTON8_APPLY, GE.MORTON8_INV))),
+        # a skewed transpose of a 200 x 130 matrix, (i, j) -> j * 200 + (i + j) % 200:
+        # no digit structure, ragged 64 x 64 boxes read in row order and
+        # written in column order
+        ("skewed transpose 200x130", L.as_layout(L.Row(200, 130)),
+         L.as_layout(L.GenPExpr([200, 130], SKEW_APPLY, SKEW_INV)),
+         OL.as_layout(OL.Row(200, 130)), OL.as_layout(GX.expr_genp([200, 130], SKEW_APPLY, SKEW_INV))),
     ]
 
 
