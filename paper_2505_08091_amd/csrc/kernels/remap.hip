@@ -20,7 +20,8 @@
 //   LEGO_FN IDX_T dst_off(IDX_T g, IDX_T q)   element offset of destination-side vector q
 // Box path (2-D maps without digit structure): a BR x BC box of the logical
 // index space is read in one order and written in another, through LDS:
-//   BR, BC, BPAD, NBC (boxes per row of boxes), EXT0, EXT1 (logical extents), NT
+//   BR, BC, BPAD, NBR x NBC (the grid of boxes), EXT0, EXT1 (logical extents), NT
+//   LEGO_FN void bord(IDX_T b, IDX_T* bi, IDX_T* bj)  box of workgroup b
 //   LEGO_FN void ws(IDX_T q, IDX_T* a, IDX_T* b)   box element read q-th
 //   LEGO_FN void wd(IDX_T q, IDX_T* a, IDX_T* b)   box element written q-th
 //   LEGO_FN IDX_T bsrc(IDX_T i, IDX_T j), bdst(IDX_T i, IDX_T j)   element
@@ -143,7 +144,9 @@ extern "C" __global__ __launch_bounds__(NT) void lego_remap_lds(const ELEM_T* __
 extern "C" __global__ __launch_bounds__(NT) void lego_remap_box(const ELEM_T* __restrict__ src,
                                                                 ELEM_T* __restrict__ dst) {
   __shared__ ELEM_T tile[BR * (BC + BPAD)];
-  const IDX_T i0 = (IDX_T)(blockIdx.x / NBC) * BR, j0 = (IDX_T)(blockIdx.x % NBC) * BC;
+  IDX_T bi, bj;
+  bord((IDX_T)blockIdx.x, &bi, &bj);
+  const IDX_T i0 = bi * BR, j0 = bj * BC;
   const bool whole = i0 + BR <= EXT0 && j0 + BC <= EXT1;
   ELEM_T v[BOX / NT];
   IDX_T slot[BOX / NT];

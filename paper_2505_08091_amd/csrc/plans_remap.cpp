@@ -242,8 +242,28 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
     }
   }
   const int NT = 256;
-  const i64 nbr = (n[0] + B - 1) / B, nbc = (n[1] + B - 1) / B;
+  const i64 nbr = (n[0] + B - 1) / B, nbc = (n[1] + B - 1) / B, nb = nbr * nbc;
   const LayoutP Ws = orders[ws].second, Wd = orders[wd].second;
+  // Box order, a layout over the grid of boxes.  A run along an antidiagonal
+  // ends mid-line at a box edge and the rest of the line belongs to the next
+  // box along the antidiagonal, so with an antidiagonal order inside boxes the
+  // boxes go in antidiagonal order too; workgroups are dispatched round-robin
+  // over the 8 XCDs, so XCD x takes the x-th eighth of that order and the
+  // boxes that share lines share its L2.
+  const bool ad_boxes = (orders[ws].first == "antidiag" || orders[wd].first == "antidiag") && nbr == nbc;
+  const bool xcd = nb % 8 == 0;
+  const LayoutP Wb = ad_boxes ? make_from_piece(make_genp(GEN_ANTIDIAG, {nbr, nbc}, {})) : make_from_piece(make_row({nbr, nbc}));
+  auto box_fn = [&](Ctx& c) {
+    int b = c.var("b", nb);
+    SymAlg al{&c};
+    Sum pos = var(c, b);
+    if (xcd) pos = add(c, mulc(c, fmod(c, var(c, b), 8), nb / 8), fdiv(c, var(c, b), 8));
+    FnSpec f;
+    f.params = {b};
+    f.outs = Wb->inv(al, pos);
+    f.out_bound = {nbr, nbc};
+    return f;
+  };
   auto order_fn = [&](const LayoutP& W) {
     return [&, W](Ctx& c) {
       int q = c.var("q", B * B);
@@ -268,13 +288,14 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
   };
   std::string info;
   bool wide = false;
-  std::string fns = emit_all({{"ws", order_fn(Ws)}, {"wd", order_fn(Wd)}, {"bsrc", addr_fn(&src)}, {"bdst", addr_fn(&dst)}},
+  std::string fns = emit_all({{"bord", box_fn}, {"ws", order_fn(Ws)}, {"wd", order_fn(Wd)}, {"bsrc", addr_fn(&src)},
+                              {"bdst", addr_fn(&dst)}},
                              &wide, &info);
   int nontemporal = 0;
   if (const char* e = std::getenv("LEGO_REMAP_NONTEMPORAL")) nontemporal = std::atoi(e);
   std::ostringstream s;
   s << header() << "#define ELEM_T " << elem_type(elem_bytes) << "\n#define IDX_T " << (wide ? "i64" : "u32")
-    << "\n#define BR " << B << "\n#define BC " << B << "\n#define BPAD " << pad << "\n#define NBC " << nbc
+    << "\n#define BR " << B << "\n#define BC " << B << "\n#define BPAD " << pad << "\n#define NBR " << nbr << "\n#define NBC " << nbc
     << "\n#define EXT0 " << n[0] << "\n#define EXT1 " << n[1] << "\n#define NT " << NT
     << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_BOX 1\n"
     << fns << "// ---- template ----\n" << tpl_remap;
@@ -287,7 +308,8 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
   R.block = NT;
   R.grid = nbr * nbc;
   R.src = s.str();
-  R.info = "box " + std::to_string(B) + "x" + std::to_string(B) + " load " + orders[ws].first + " (" +
+  R.info = "box " + std::to_string(B) + "x" + std::to_string(B) + (ad_boxes ? " antidiag" : " row") +
+           (xcd ? "-xcd" : "") + " order load " + orders[ws].first + " (" +
            std::to_string(bs) + " runs) store " + orders[wd].first + " (" + std::to_string(bd) + " runs) pad " +
            std::to_string(pad) + " NT=" + std::to_string(NT) + info;
   return true;

@@ -74,11 +74,15 @@ int main(int argc, char** argv) {
   const u64 n = (u64)EXT0 * EXT1, nsrc = n;
   if ((BR * BC) % NT || NT > 256) FAIL("NT does not divide the box");
   if ((unsigned long long)BR * (BC + BPAD) * sizeof(ELEM_T) > 65536) FAIL("box exceeds 64 KiB of LDS");
-  const u64 nbr = (EXT0 + BR - 1) / BR;
+  if (NBR != (EXT0 + BR - 1) / BR || NBC != (EXT1 + BC - 1) / BC) FAIL("box grid does not cover the extents");
   std::vector<long long> perm(n, -2);
   std::vector<long long> tile((u64)BR * (BC + BPAD));
-  for (u64 bx = 0; bx < nbr * NBC; ++bx) {
-    const u64 i0 = (bx / NBC) * BR, j0 = (bx % NBC) * BC;
+  std::vector<char> bseen((u64)NBR * NBC);
+  for (u64 bx = 0; bx < (u64)NBR * NBC; ++bx) {
+    IDX_T bi, bj;
+    bord((IDX_T)bx, &bi, &bj);
+    if (bi >= NBR || bj >= NBC || bseen[(u64)bi * NBC + bj]++) FAIL("bord is not a bijection onto the boxes");
+    const u64 i0 = (u64)bi * BR, j0 = (u64)bj * BC;
     std::fill(tile.begin(), tile.end(), -1);
     std::vector<char> rseen(BR * BC), wseen(BR * BC);
     for (u64 q = 0; q < (u64)BR * BC; ++q) {
