@@ -48,7 +48,7 @@ enum {
   LEGO_E_NOT_PERMUTATION = -3,/* sigma is not a permutation of [1..d] */
   LEGO_E_OUT_OF_RANGE = -4,   /* an index outside the layout's space */
   LEGO_E_NOT_BIJECTIVE = -5,  /* brute-force check found a collision or a gap */
-  LEGO_E_UNSUPPORTED = -6,    /* valid request this build does not implement */
+  LEGO_E_UNSUPPORTED = -6,    /* valid request the library does not implement */
   LEGO_E_JIT = -7,            /* run-time compilation of a generated kernel failed */
   LEGO_E_HIP = -8,            /* a HIP runtime call failed */
   LEGO_E_NO_MEMORY = -9
