@@ -141,12 +141,15 @@ LEGO_FN u64 lego_isqrt_u64(u64 v) {
 }
 // 32-bit operands: the square root of the nearest float, corrected to the
 // exact floor by integer comparisons (the estimate is off by at most one for
-// every 32-bit v; the loops make the result exact whatever the estimate).
+// every 32-bit v; the loops make the result exact whatever the estimate).  The
+// floor is at most 65535, so clamping the estimate there keeps every square
+// in 32 bits.
 LEGO_FN u32 lego_isqrt(u32 v) {
-  u64 r = (u64)__builtin_sqrtf((float)v);
+  u32 r = (u32)__builtin_sqrtf((float)v);
+  r = r < 65535u ? r : 65535u;
   while (r * r > v) --r;
-  while ((r + 1) * (r + 1) <= v) ++r;
-  return (u32)r;
+  while (r < 65535u && (r + 1) * (r + 1) <= v) ++r;
+  return r;
 }
 LEGO_FN i64 lego_isqrt(i64 v) { return v <= 0 ? 0 : (i64)lego_isqrt_u64((u64)v); }
 )PRELUDE";
