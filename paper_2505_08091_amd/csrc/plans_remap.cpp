@@ -553,7 +553,12 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   // together (run 1, a transpose: 512-byte runs on both sides of a 128x128
   // fp32 tile, +9-13% over 32 KiB on the 8192^2 fp32 transpose); smaller
   // remaps keep 16 KiB tiles in destination order.
-  const bool hbm_bound = 2 * N * elem_bytes > (256ll << 20);
+  // A map that keeps no two neighbours together (run 1) takes the large
+  // source-order tiles also below that size once they still give every CU
+  // four tiles (4096^2 fp32 transpose: 4.89/5.34 -> 5.32/6.11 TB/s; at 2048^2,
+  // 256 such tiles, the 16 KiB tiles stay ahead).
+  const bool hbm_bound =
+      2 * N * elem_bytes > (256ll << 20) || (run == 1 && N * elem_bytes >= 1024ll * 64 * 1024);
   i64 tile_bytes = hbm_bound ? (run == 1 ? 64 * 1024 : 32 * 1024) : 16 * 1024;
   if (const char* e = std::getenv("LEGO_REMAP_TILE_BYTES")) tile_bytes = std::max<i64>(256, std::atoll(e));
   const i64 max_tile = std::min<i64>(N, std::max<i64>(32 * 1024, tile_bytes) / elem_bytes);
