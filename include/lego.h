@@ -127,6 +127,13 @@ lego_status lego_piece_dims(lego_piece_t p, int* rank, int64_t* dims);
  * Errors: INVALID_ARG. */
 lego_status lego_groupby(int rank, const int64_t* dims, lego_layout_t* out);
 
+/* GroupBy(T^1..T^q) over q tile levels of d dimensions each (Figure 3's
+ * grammar names the levels): tiles[q*d], level-major.  The logical index is
+ * the concatenation of the levels' coordinates (q*d entries), so this is
+ * lego_groupby(q*d, tiles) with the level structure checked.  Errors:
+ * INVALID_ARG (q < 1, d < 1, q*d > 64, null, size <= 0). */
+lego_status lego_groupby_tiles(int q, int d, const int64_t* tiles, lego_layout_t* out);
+
 /* base.OrderBy(P_1..P_n) (Equation (2) dot notation): appends a reordering; the
  * chain is applied in call order by apply.  Errors: INVALID_ARG,
  * SIZE_MISMATCH (element counts differ). */
@@ -139,9 +146,10 @@ lego_status lego_tileby(int q, int d, const int64_t* tiles, lego_layout_t* out);
 
 /* TileOrderBy_{q x d}(P^1..P^q): logical index = full coordinates (extents
  * N_k = prod_h n^h_k); apply gives the position in tile-major storage whose
- * level h is ordered by piece P^h.  (The printed definition is garbled; this
- * is the reading that maps full coordinates to hierarchically tiled storage.) */
-lego_status lego_tileorderby(int q, const lego_piece_t* levels, lego_layout_t* out);
+ * level h is ordered by piece P^h, each of rank d.  (The printed definition is
+ * garbled; this is the reading that maps full coordinates to hierarchically
+ * tiled storage.)  Errors: INVALID_ARG (q < 1, null, a level not of rank d). */
+lego_status lego_tileorderby(int q, int d, const lego_piece_t* levels, lego_layout_t* out);
 
 /* GroupBy(P.dims).OrderBy(P): a single permutation used as a whole layout. */
 lego_status lego_layout_from_piece(lego_piece_t p, lego_layout_t* out);
@@ -242,6 +250,11 @@ typedef struct {
   int wm, wn;            /* wave tile; 0 = default (bm/2, bn/2) */
   int group_m;           /* grouping of the default schedule; 0 = 8 */
   int xcd_remap;         /* 1 = keep consecutive scheduled tiles on one XCD */
+  int stages;            /* LDS stages of the k loop (2..4, within 160 KiB of LDS);
+                            0 = chosen; a count the plan cannot use is UNSUPPORTED */
+  int max_workgroups;    /* plans whose workgroups walk several tiles (the plan
+                            text says "persistent"): launch at most this many
+                            workgroups; 0 = as many as the device holds at once */
   lego_layout_t a, b, c, sched, lds_a, lds_b;
   lego_layout_t frag_a, frag_b, frag_c;  /* MFMA fragment layouts (see below); NULL: chosen */
 } lego_gemm_desc;

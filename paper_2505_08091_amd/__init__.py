@@ -45,7 +45,7 @@ class lego_gemm_desc(ctypes.Structure):  # noqa: N801 (C name)
     _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
                 ("in_dtype", ctypes.c_int), ("bm", ctypes.c_int), ("bn", ctypes.c_int), ("bk", ctypes.c_int),
                 ("wm", ctypes.c_int), ("wn", ctypes.c_int), ("group_m", ctypes.c_int), ("xcd_remap", ctypes.c_int),
-                ("a", _vp), ("b", _vp), ("c", _vp), ("sched", _vp), ("lds_a", _vp), ("lds_b", _vp),
+                ("stages", ctypes.c_int), ("max_workgroups", ctypes.c_int), ("a", _vp), ("b", _vp), ("c", _vp), ("sched", _vp), ("lds_a", _vp), ("lds_b", _vp),
                 ("frag_a", _vp), ("frag_b", _vp), ("frag_c", _vp)]
 
 
@@ -61,9 +61,10 @@ _SIGS = {
     "lego_genp_expr": ([ctypes.c_int, c_i64p, ctypes.c_char_p, ctypes.c_char_p, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_piece_dims": ([_vp, ctypes.POINTER(ctypes.c_int), c_i64p], ctypes.c_int),
     "lego_groupby": ([ctypes.c_int, c_i64p, ctypes.POINTER(_vp)], ctypes.c_int),
+    "lego_groupby_tiles": ([ctypes.c_int, ctypes.c_int, c_i64p, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_orderby": ([_vp, ctypes.c_int, ctypes.POINTER(_vp), ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_tileby": ([ctypes.c_int, ctypes.c_int, c_i64p, ctypes.POINTER(_vp)], ctypes.c_int),
-    "lego_tileorderby": ([ctypes.c_int, ctypes.POINTER(_vp), ctypes.POINTER(_vp)], ctypes.c_int),
+    "lego_tileorderby": ([ctypes.c_int, ctypes.c_int, ctypes.POINTER(_vp), ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_layout_from_piece": ([_vp, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_expandby": ([ctypes.c_int, c_i64p, c_i64p, _vp, ctypes.POINTER(_vp)], ctypes.c_int),
     "lego_layout_rank": ([_vp, ctypes.POINTER(ctypes.c_int)], ctypes.c_int),
@@ -277,6 +278,17 @@ def GroupBy(*tiles):  # noqa: N802
     return Layout(out)
 
 
+def GroupByTiles(*tiles):  # noqa: N802
+    """GroupBy over q tile levels of equal rank d (lego_groupby_tiles)."""
+    q, d = len(tiles), len(tiles[0])
+    flat = [int(x) for t in tiles for x in t]
+    if any(len(t) != d for t in tiles):
+        raise LegoError(-1, "GroupBy tile levels must have equal rank")
+    out = ctypes.c_void_p()
+    _check(_lib.lego_groupby_tiles(q, d, _i64(flat), ctypes.byref(out)))
+    return Layout(out)
+
+
 def TileBy(*tiles):  # noqa: N802
     q, d = len(tiles), len(tiles[0])
     if any(len(t) != d for t in tiles):
@@ -290,7 +302,15 @@ def TileBy(*tiles):  # noqa: N802
 def TileOrderBy(*pieces):  # noqa: N802
     arr = (ctypes.c_void_p * len(pieces))(*[p.h for p in pieces])
     out = ctypes.c_void_p()
-    _check(_lib.lego_tileorderby(len(pieces), arr, ctypes.byref(out)))
+    _check(_lib.lego_tileorderby(len(pieces), len(pieces[0].dims()), arr, ctypes.byref(out)))
+    return Layout(out)
+
+
+def _tileorderby_d(d, *pieces):
+    """lego_tileorderby with an explicit level rank d (tests of its check)."""
+    arr = (ctypes.c_void_p * len(pieces))(*[p.h for p in pieces])
+    out = ctypes.c_void_p()
+    _check(_lib.lego_tileorderby(len(pieces), int(d), arr, ctypes.byref(out)))
     return Layout(out)
 
 
@@ -354,11 +374,13 @@ def remap_plan(src_layout, dst_layout, elem_bytes):
 
 
 def _desc(M, N, K, dtype, a=None, b=None, c=None, sched=None, lds_a=None, lds_b=None, bm=0, bn=0, bk=0, wm=0, wn=0,
-          group_m=0, xcd_remap=1, frag_a=None, frag_b=None, frag_c=None):
+          group_m=0, xcd_remap=1, stages=0, max_workgroups=0, frag_a=None, frag_b=None, frag_c=None):
     d = lego_gemm_desc()
     d.M, d.N, d.K = int(M), int(N), int(K)
     d.in_dtype = DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
     d.bm, d.bn, d.bk, d.wm, d.wn, d.group_m, d.xcd_remap = bm, bn, bk, wm, wn, group_m, xcd_remap
+    d.stages = stages
+    d.max_workgroups = max_workgroups
     for name, lay in (("a", a), ("b", b), ("c", c), ("sched", sched), ("lds_a", lds_a), ("lds_b", lds_b),
                       ("frag_a", frag_a), ("frag_b", frag_b), ("frag_c", frag_c)):
         setattr(d, name, lay.h if lay is not None else None)

@@ -108,7 +108,7 @@ void hip_check(hipError_t e, const char* what) {
   if (e != hipSuccess) throw HipFailure(std::string(what) + ": " + hipGetErrorString(e));
 }
 
-void launch(const KernelPlan& k, void** args, void* stream) {
+void launch(const KernelPlan& k, void** args, void* stream, long long max_wgs = 0) {
   if (k.grid <= 0 || k.grid > 0x7fffffffll) throw Unsupported("grid too large");
   int dev = 0;
   hip_check(hipGetDevice(&dev), "hipGetDevice");
@@ -125,8 +125,32 @@ void launch(const KernelPlan& k, void** args, void* stream) {
       k.fns.fn[dev] = (void*)fn;
     }
   }
-  hip_check(hipModuleLaunchKernel(fn, (unsigned)k.grid, 1, 1, (unsigned)k.block, 1, 1, 0, (hipStream_t)stream,
-                                  args, nullptr),
+  long long grid = k.grid;
+  if (k.persistent) {
+    // A persistent kernel walks its tiles grid-stride: launch as many
+    // workgroups as the device holds at once (every CU busy, no second wave
+    // of workgroups), never more than there are tiles.
+    long long res = 0;
+    if (slot) {
+      std::lock_guard<std::mutex> lk(k.fns.mu);
+      res = k.fns.resident[dev];
+    }
+    if (!res) {
+      int per_cu = 0, cus = 0;
+      hip_check(hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, k.block, 0),
+                "hipModuleOccupancyMaxActiveBlocksPerMultiprocessor");
+      hip_check(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev), "hipDeviceGetAttribute");
+      res = (long long)std::max(1, per_cu) * std::max(1, cus);
+      if (slot) {
+        std::lock_guard<std::mutex> lk(k.fns.mu);
+        k.fns.resident[dev] = res;
+      }
+    }
+    grid = std::min(grid, res);
+    if (max_wgs > 0) grid = std::min(grid, max_wgs);
+  }
+  hip_check(hipModuleLaunchKernel(fn, (unsigned)grid, 1, 1, (unsigned)k.block, 1, 1, 0, (hipStream_t)stream, args,
+                                  nullptr),
             "hipModuleLaunchKernel");
 }
 
@@ -260,11 +284,22 @@ lego_status lego_tileby(int q, int d, const int64_t* tiles, lego_layout_t* out) 
   });
 }
 
-lego_status lego_tileorderby(int q, const lego_piece_t* levels, lego_layout_t* out) {
+lego_status lego_groupby_tiles(int q, int d, const int64_t* tiles, lego_layout_t* out) {
+  return guard([&] {
+    if (q < 1 || d < 1 || q * d > 64 || !tiles) throw std::invalid_argument("bad GroupBy tile shape");
+    return out_layout(make_groupby(dims_arg(q * d, tiles, 64)), out);
+  });
+}
+
+lego_status lego_tileorderby(int q, int d, const lego_piece_t* levels, lego_layout_t* out) {
   return guard([&] {
     if (q < 1 || !levels) throw std::invalid_argument("TileOrderBy needs at least one level");
+    if (d < 1 || q * d > 64) throw std::invalid_argument("bad TileOrderBy shape");
     std::vector<PieceP> ps;
-    for (int k = 0; k < q; ++k) ps.push_back(piece_of(levels[k]));
+    for (int k = 0; k < q; ++k) {
+      ps.push_back(piece_of(levels[k]));
+      if ((int)ps.back()->n.size() != d) throw std::invalid_argument("a TileOrderBy level is not of rank d");
+    }
     return out_layout(make_tileorderby(ps), out);
   });
 }
@@ -503,7 +538,8 @@ lego_status lego_gemm(const lego_gemm_desc* desc, const void* d_a, const void* d
     void* a = const_cast<void*>(d_a);
     void* b = const_cast<void*>(d_b);
     void* args[] = {&a, &b, &d_c};
-    launch(*plan, args, stream);
+    if (desc->max_workgroups < 0) throw std::invalid_argument("max_workgroups must not be negative");
+    launch(*plan, args, stream, desc->max_workgroups);
     return LEGO_OK;
   });
 }

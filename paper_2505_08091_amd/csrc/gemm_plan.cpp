@@ -10,6 +10,7 @@
 
 #include "errors.hpp"
 #include "lower.hpp"
+#include "tune.hpp"
 
 namespace lego {
 
@@ -41,6 +42,7 @@ GemmRequest gemm_request(const lego_gemm_desc& d, const std::function<LayoutP(le
   r.wn = d.wn;
   r.group_m = d.group_m;
   r.xcd = d.xcd_remap;
+  r.stages = d.stages;
   r.a = resolve(d.a);
   r.b = resolve(d.b);
   r.c = resolve(d.c);
@@ -82,7 +84,7 @@ bool same_map(const Layout& x, const Layout& y) {
 LayoutP default_lds(i64 rows, i64 k) {
   if (k % 8 == 0 && pow2(k / 8) && k / 8 >= 2) {
     i64 s = std::max<i64>(1, 128 / k);
-    if (const char* e = std::getenv("LEGO_GEMM_LDS_S")) s = std::max(1, std::atoi(e));
+    s = std::max<i64>(1, tune("gemm.lds_s", s));
     return make_from_piece(make_genp(GEN_XOR_SWIZZLE, {rows, k}, {8, s}));
   }
   return make_from_piece(make_row({rows, k}));
@@ -176,7 +178,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // [M, N] are dropped.
   const bool edge_m = M % bm != 0, edge_n = N % bn != 0, edge_k = K % bk != 0;
   int MB = (wm % 32 == 0 && wn % 32 == 0) ? 32 : 16;
-  if (const char* e = std::getenv("LEGO_GEMM_MFMA")) MB = std::atoi(e) == 16 ? 16 : MB;
+  MB = tune("gemm.mfma", MB) == 16 ? 16 : MB;
   {
     // Given fragment layouts select the instruction whose fragments they are.
     int want = -1;
@@ -445,7 +447,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // Direct global-to-LDS copies need 16-byte global runs under the inverse
   // LDS layout and whole rounds of load vectors.
   bool direct = true;
-  if (const char* e = std::getenv("LEGO_GEMM_DIRECT")) direct = std::atoi(e) != 0;
+  direct = tune("gemm.direct", 1) != 0;
   if ((bk / KB) % 2) direct = false;  // the direct loop alternates fragment buffers per substep
   for (Operand& o : ops) {
     if (!direct) break;
@@ -491,13 +493,18 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   int nstages = 2;
   if (direct) {
     nstages = (int)std::min<i64>(4, (160 * 1024) / stage_bytes);
-    if (const char* e = std::getenv("LEGO_GEMM_STAGES")) nstages = std::atoi(e);
-    nstages = (int)std::max<i64>(2, std::min<i64>(nstages, (160 * 1024) / stage_bytes));
     // the waits count loads: NSTAGES-1 tiles behind the awaited one must fit vmcnt's 63
     const i64 per_tile = ops[0].NV + ops[1].NV;
     while (nstages > 2 && (nstages - 1) * per_tile > 63) --nstages;
     if (per_tile > 63) direct = false;
+    if (rq.stages) {
+      if (rq.stages < 2 || rq.stages > 4 || rq.stages * stage_bytes > 160 * 1024 || (rq.stages - 1) * per_tile > 63)
+        throw Unsupported("this many LDS stages do not fit the LDS or the load counter");
+      nstages = rq.stages;
+    }
   }
+  // Register-staged plans double-buffer the LDS tile.
+  if (!direct && rq.stages && rq.stages != 2) throw Unsupported("register-staged plans use two LDS stages");
 
   // ----- emit the index functions
   using Builder = std::function<FnSpec(Ctx&)>;
@@ -767,43 +774,52 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // Two staging register sets when the accumulators live in AGPRs (one wave
   // per SIMD leaves the VGPRs for them); one otherwise, so two waves fit.
   int prefetch = (MI * NI * NREG > 128) ? 2 : 1;
-  if (const char* e = std::getenv("LEGO_GEMM_PREFETCH")) prefetch = std::atoi(e) == 2 ? 2 : 1;
+  prefetch = tune("gemm.prefetch", prefetch) == 2 ? 2 : 1;
   if (Kt < 2) prefetch = 1;
   // Register-staged plans use the rolling pipeline (one staging set; LDS
   // writes and reloads spread over the substeps): measured +7% on the 8192^3
   // bf16 GEMM and +16% on the 4096^3 Morton-A GEMM over staging the whole
   // tile in one substep.
   int rolling = 1;
-  if (const char* e = std::getenv("LEGO_GEMM_ROLLING")) rolling = std::atoi(e) != 0;
+  rolling = tune("gemm.rolling", rolling) != 0;
   // The direct copies of the next tile go out between MFMA rows rather than
   // in one burst (measured 0.87 -> 0.85 ms on the 8192^3 bf16 GEMM with
   // 128x128 wave tiles, and 0.870 -> 0.864 ms with 8 waves of 128x64).
   int dma_spread = 1;
-  if (const char* e = std::getenv("LEGO_GEMM_DMA_SPREAD")) dma_spread = std::atoi(e) != 0;
+  dma_spread = tune("gemm.dma_spread", dma_spread) != 0;
   // Direct-copy plans read fragments two substeps ahead of their MFMAs, so
   // that reads held up by copies landing in LDS do not stall them (0.857 ->
   // 0.852 ms on the 8192^3 bf16 GEMM); not with the transposing reads, whose
   // wait at each substep covers every read in flight.
   int frag_dist = (ops[0].frtr || ops[1].frtr) ? 1 : 2;
-  if (const char* e = std::getenv("LEGO_GEMM_FRAG_DIST")) frag_dist = std::max(1, std::min(2, std::atoi(e)));
+  frag_dist = (int)std::max<long long>(1, std::min<long long>(3, tune("gemm.frag_dist", frag_dist)));
   // (Reads two substeps ahead need three substeps per step: with two, the
   // early reads of the last substep would replace fragments its later MFMA
   // rows still use.)
   if (!direct || bk / KB <= frag_dist) frag_dist = 1;
+  if (const long long rows = tune("gemm.dma_rows", 0)) s << "#define DMA_ROWS " << rows << "\n";
+  // Loop unrolled over the LDS ring when one wave per SIMD leaves the
+  // registers for per-stage fragment addresses.
+  const int ring_unroll = (int)tune("gemm.ring_unroll", MI * NI * NREG > 128 ? 1 : 0);
+  s << "#define RING_UNROLL " << ring_unroll << "\n";
   s << "#define PREFETCH " << prefetch << "\n#define ROLLING " << rolling << "\n#define DMA_SPREAD " << dma_spread
     << "\n#define FRAG_DIST " << frag_dist << "\n#define DIRECT_LDS " << (direct ? 1 : 0)
     << "\n#define NSTAGES " << nstages << "\n";
-  const char* store_env = std::getenv("LEGO_GEMM_STORE_AT");
-  int store_at = store_env ? std::atoi(store_env) : (bk / KB) / 2;
+  int store_at = (int)tune("gemm.store_at", (bk / KB) / 2);
   store_at = std::max(0, std::min(store_at, bk / KB - 1));
   s << "#define STORE_AT " << store_at << "\n";
-  s << "#define C_SEP " << (csep ? 1 : 0) << "\n" << code << "// ---- template ----\n" << tpl_gemm;
+  // A persistent grid walks several tiles per workgroup, chaining the LDS
+  // ring across tiles: the first steps of the next tile are requested during
+  // the last NSTAGES steps of the current one, so a tile needs that many.
+  const bool persist = direct && Kt >= nstages && tune("gemm.persist", 1) != 0;
+  s << "#define C_SEP " << (csep ? 1 : 0) << "\n#define PERSIST " << (persist ? 1 : 0) << "\n" << code << "// ---- template ----\n" << tpl_gemm;
 
   GemmPlan g;
   g.src = s.str();
   g.kernel = "lego_gemm";
   g.grid = P;
   g.block = NT;
+  g.persistent = persist;
   std::ostringstream info;
   info << "gemm " << M << "x" << N << "x" << K << (rq.dtype == LEGO_BF16 ? " bf16" : " f16") << " tile " << bm << "x"
        << bn << "x" << bk << " waves " << NWM << "x" << NWN << " wave " << wm << "x" << wn << " mfma " << MB << "x"
@@ -817,7 +833,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
        << (direct ? " direct-lds" : " staged")
        << (direct ? std::string(dma_spread ? " spread" : " burst") + " fd" + std::to_string(frag_dist) : "")
        << (ragged_groups ? " ragged-groups" : "")
-       << (ops[0].edge || ops[1].edge || cedge ? " edges" : "") << " stages " << nstages << " lds " << nstages * stage_bytes
+       << (ops[0].edge || ops[1].edge || cedge ? " edges" : "") << (persist ? " persistent" : "") << " stages " << nstages << " lds " << nstages * stage_bytes
        << "B ops" << opsinfo.str();
   g.info = info.str();
   g.direct_vec = direct && ops[0].frvec && ops[1].frvec;
@@ -845,7 +861,7 @@ std::map<std::string, std::pair<std::vector<LayoutP>, std::shared_ptr<GemmPlan>>
 std::shared_ptr<GemmPlan> gemm_plan_cached(const GemmRequest& rq) {
   std::ostringstream k;
   k << rq.M << "," << rq.N << "," << rq.K << "," << rq.dtype << "," << rq.bm << "," << rq.bn << "," << rq.bk << ","
-    << rq.wm << "," << rq.wn << "," << rq.group_m << "," << rq.xcd;
+    << rq.wm << "," << rq.wn << "," << rq.group_m << "," << rq.xcd << "," << rq.stages;
   for (auto* l : {&rq.a, &rq.b, &rq.c, &rq.sched, &rq.lds_a, &rq.lds_b, &rq.frag_a, &rq.frag_b, &rq.frag_c})
     k << "," << (const void*)l->get();
   std::string key = k.str();
@@ -905,6 +921,18 @@ std::vector<std::pair<std::string, std::string>> selftest_sources() {
   g5.b = r4;
   g5.xcd = 1;
   out.push_back({"gemm 4096^3 f16 morton A, row B", plan_gemm(g5).src});
+  // Operands contiguous along m or n: fragments through the transposing LDS
+  // load (B row-major: B only; A column-major too: both).
+  LayoutP c4 = make_from_piece(make_col({4096, 4096}));
+  for (int both = 0; both < 2; ++both) {
+    GemmRequest g6;
+    g6.M = g6.N = g6.K = 4096;
+    g6.dtype = LEGO_F16;
+    g6.a = both ? c4 : r4;
+    g6.b = r4;
+    g6.xcd = 1;
+    out.push_back({both ? "gemm 4096^3 f16 col A, row B" : "gemm 4096^3 f16 row A, row B", plan_gemm(g6).src});
+  }
   return out;
 }
 

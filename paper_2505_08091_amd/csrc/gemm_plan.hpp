@@ -18,6 +18,7 @@ struct GemmRequest {
   i64 M = 0, N = 0, K = 0;
   int dtype = LEGO_BF16;
   int bm = 0, bn = 0, bk = 0, wm = 0, wn = 0, group_m = 0, xcd = 0;
+  int stages = 0;  // LDS stages; 0: chosen
   LayoutP a, b, c, sched, lds_a, lds_b;  // null: defaults
   LayoutP frag_a, frag_b, frag_c;        // null: chosen; else they select the MFMA instruction
 };

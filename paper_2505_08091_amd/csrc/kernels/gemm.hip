@@ -114,6 +114,11 @@ LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
 #ifndef FRAG_DIST
 #define FRAG_DIST 1
 #endif
+// MFMA rows after the stage barrier over which the copies of a step are
+// spread.
+#ifndef DMA_ROWS
+#define DMA_ROWS (FRAG_DIST * MFMA_ROWS)
+#endif
 #if (BK / KB) % (FRAG_DIST + 1) == 0
 #define NFB (FRAG_DIST + 1)
 #else
@@ -171,6 +176,32 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = (acc_t){};
+  // The accumulators of tile (tm_, tn_) to C, with non-temporal stores (C is
+  // not read again; measured ahead of ordinary stores).  Each store writes
+  // 2 rows of 32 consecutive C elements of an MFMA block (the 32x32 C
+  // fragment layout); 16-byte stores of 4 consecutive elements from
+  // operand-swapped MFMAs write 32-byte pieces of 32 rows and measured 20%
+  // slower on the 8192^3 bf16 GEMM.
+  auto store_c = [&](IDX_T tm_, IDX_T tn_) {
+#if C_SEP
+    float* __restrict__ Cb = C + c_t(tm_, tn_);
+#endif
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int r = 0; r < NREG; ++r) {
+#if C_EDGE
+          if (!c_ok(tm_, tn_, lane, w, i, j, r)) continue;
+#endif
+#if C_SEP
+          __builtin_nontemporal_store(acc[i][j][r], Cb + c_l(lane, w, i, j, r));
+#else
+          __builtin_nontemporal_store(acc[i][j][r], C + c_f(tm_, tn_, lane, w, i, j, r));
+#endif
+        }
+  };
 
   // Load vectors [lo, hi) of the tile for step kt (A's A_NV vectors, then
   // B's B_NV) into staging set rbuf.
@@ -289,6 +320,18 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     }
   };
 
+  // Row r of the MFMAs of one substep with fragment set fb: every MFMA of a
+  // row has the same first operand, A's fragment r.
+#define MFMA_ROWS MI
+  auto mfma_row = [&](int r, int fb) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) acc[r][j] = MFMA(af[fb][r], bf[fb][j], acc[r][j]);
+  };
+  auto mfma_all = [&](int fb) {
+#pragma unroll
+    for (int r = 0; r < MFMA_ROWS; ++r) mfma_row(r, fb);
+  };
+
   // One K step on LDS stage kt&1.  `lbuf`: staging set receiving tile
   // kt+PREFETCH; `sbuf`: staging set holding tile kt+1, written to the other
   // LDS stage during the step.  The stage being written was last read in
@@ -308,10 +351,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);
       if (s == STORE_AT && kt + 1 < KT) sstore(cur ^ 1, sbuf);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      mfma_all(s & 1);
       if (s == STORE_AT) {
         // Spread the LDS stores between the MFMAs of this substep.
 #pragma unroll
@@ -330,9 +370,16 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // LDS base + 16 * lane, so load vector q = u*NT + tid fills LDS slot q; the
   // planner gave that lane the global address of the logical element the LDS
   // layout puts in slot q (the inverse of the LDS layout drives the copy).
-  // NSTAGES LDS stages form a ring: the tile for step kt+NSTAGES is
-  // requested during step kt, right after the barrier of its last substep,
-  // into the stage step kt has just finished reading.
+  // NSTAGES LDS stages form a ring over the k-steps: the tile for step
+  // g+NSTAGES is requested during step g, right after the barrier of its last
+  // substep, into the stage step g has just finished reading.
+  //
+  // The grid is persistent when the launch makes it so (fewer workgroups than
+  // output tiles): workgroup b computes the tiles whose schedule index is b,
+  // b + G, b + 2G, ... (G = gridDim.x, every workgroup on the XCD that b is
+  // dispatched to).  The ring runs on across tile boundaries: the last steps
+  // of one tile request the first steps of the next, so the C stores of a
+  // tile are issued while the next tile's operands are already on the way.
   const IDX_T wu = __builtin_amdgcn_readfirstlane(tid / 64u);
 #if A_BUF || B_BUF
   // Range-checked buffer loads: an offset past the buffer's end (0xFFFFFFFF
@@ -340,26 +387,53 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)A_BYTES, 0x00020000);
   const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)B, (short)0, (int)B_BYTES, 0x00020000);
 #endif
-  // Copies [lo, hi) of the tile for step kt (A's A_NV vectors, then B's).
-  auto dload_part = [&](IDX_T kt, int stage, int lo, int hi) {
+  // One output tile: its coordinates and operand bases.
+  struct Tile {
+    IDX_T tm, tn;
+    const elem_t* ab;
+    const elem_t* bb;
+  };
+  auto tile_of = [&](IDX_T p) {
+    Tile t;
+    sched(p, &t.tm, &t.tn);
+#if A_SEP
+    t.ab = A + a_gt(t.tm);
+#else
+    t.ab = A;
+#endif
+#if B_SEP
+    t.bb = B + b_gt(t.tn);
+#else
+    t.bb = B;
+#endif
+    return t;
+  };
+  // Copies [lo, hi) of step kt of tile t (A's A_NV vectors, then B's).
+  auto dload_part = [&](const Tile& t, IDX_T kt, int stage, int lo, int hi) {
     elem_t* la = lds + stage * STAGE;
     elem_t* lb = la + A_STAGE;
 #pragma unroll
     for (int u = 0; u < A_NV; ++u) {
       if (u < lo || u >= hi) continue;
 #if A_SEP
-      const elem_t* src = Ab + a_gk(kt) + a_loc[u];
+      const elem_t* src = t.ab + a_gk(kt) + a_loc[u];
 #else
-      const elem_t* src = A + a_gf(tm, kt, tid, u);
+      const elem_t* src = A + a_gf(t.tm, kt, tid, u);
 #endif
       __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(la + ((IDX_T)u * NT + wu * 64u) * 8u);
 #if A_BUF
 #if A_EDGE
-      const unsigned off = a_ok(tm, kt, tid, u) ? (unsigned)((src - A) * 2) : 0xFFFFFFFFu;
-#else
-      const unsigned off = (unsigned)((src - A) * 2);
-#endif
+      const unsigned off = a_ok(t.tm, kt, tid, u) ? (unsigned)((src - A) * 2) : 0xFFFFFFFFu;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, dst, 16, off, 0, 0, 0);
+#elif A_SEP
+      // The lane's byte offset is fixed; the tile and k-step part is one
+      // scalar offset, so a copy costs no vector arithmetic.
+      (void)src;
+      const unsigned soff = (unsigned)((t.ab - A) + a_gk(kt)) * 2u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, dst, 16, a_loc[u] * 2u, soff, 0, 0);
+#else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, dst, 16, (unsigned)((src - A) * 2), 0, 0, 0);
+#endif
 #else
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src, dst, 16, 0, 0);
 #endif
@@ -368,24 +442,27 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     for (int u = 0; u < B_NV; ++u) {
       if (A_NV + u < lo || A_NV + u >= hi) continue;
 #if B_SEP
-      const elem_t* src = Bb + b_gk(kt) + b_loc[u];
+      const elem_t* src = t.bb + b_gk(kt) + b_loc[u];
 #else
-      const elem_t* src = B + b_gf(tn, kt, tid, u);
+      const elem_t* src = B + b_gf(t.tn, kt, tid, u);
 #endif
       __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(lb + ((IDX_T)u * NT + wu * 64u) * 8u);
 #if B_BUF
 #if B_EDGE
-      const unsigned off = b_ok(tn, kt, tid, u) ? (unsigned)((src - B) * 2) : 0xFFFFFFFFu;
-#else
-      const unsigned off = (unsigned)((src - B) * 2);
-#endif
+      const unsigned off = b_ok(t.tn, kt, tid, u) ? (unsigned)((src - B) * 2) : 0xFFFFFFFFu;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, off, 0, 0, 0);
+#elif B_SEP
+      (void)src;
+      const unsigned soff = (unsigned)((t.bb - B) + b_gk(kt)) * 2u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, b_loc[u] * 2u, soff, 0, 0);
+#else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, (unsigned)((src - B) * 2), 0, 0, 0);
+#endif
 #else
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src, dst, 16, 0, 0);
 #endif
     }
   };
-  auto dload = [&](IDX_T kt, int stage) { dload_part(kt, stage, 0, A_NV + B_NV); };
   // s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt at their maxima).
 #define VMCNT_WAIT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | 0x70 | 0xF00)
   // Wait until at most `after` tiles of direct loads are still in flight.
@@ -400,85 +477,73 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     else VMCNT_WAIT(3 * (A_NV + B_NV));  // (waits longer than needed beyond 3)
 #endif
   };
-  // Every stage of the ring is filled up front; afterwards the tile for step
-  // kt+NSTAGES is requested as soon as the barrier of step kt has retired the
-  // last reader of its stage (a substep before step kt+1 begins).
+  const IDX_T ntiles = (IDX_T)(GEMM_MT * GEMM_NT);
+  IDX_T pid = blockIdx.x;
+  Tile cur = tile_of(pid);
+  // Every stage of the ring is filled up front; afterwards step g+NSTAGES is
+  // requested as soon as the barrier of step g has retired the last reader of
+  // its stage (a substep before step g+1 begins).  Every step requests one
+  // step's copies (with fewer k-steps than stages, repeats of the tile's
+  // steps), so the number in flight at each barrier is always the same.
 #pragma unroll
-  for (int p = 0; p < NSTAGES; ++p)
-    if ((IDX_T)p < KT) dload(p, p);
-  wait_tiles((int)(KT - 1 < (IDX_T)(NSTAGES - 1) ? KT - 1 : (IDX_T)(NSTAGES - 1)));
+  for (int p = 0; p < NSTAGES; ++p) dload_part(cur, (IDX_T)p % KT, p, 0, A_NV + B_NV);
+  wait_tiles(NSTAGES - 1);
   __syncthreads();
   // Fragments are read FRAG_DIST substeps ahead of their MFMAs; the barrier
   // that hands over the LDS stages sits FRAG_DIST substeps before the end of
   // a step, so reads of the next stage can start there.
 #pragma unroll
   for (int p = 0; p < FRAG_DIST; ++p) fload(lds, lds + A_STAGE, p, p % NFB);
-  // One K step.  MORE (a compile-time flag): tile kt+NSTAGES exists.  The
-  // loop is peeled into steps with and without it so that the body of each
-  // has no branch: a branch would keep the scheduler from placing the copies
-  // and the fragment reads between the MFMAs.
-  auto kstep = [&](IDX_T kt, auto more) {
-    constexpr bool MORE = decltype(more)::value;
+  // One K step on LDS stage `cur_stage`; during it, step ck of tile `ct` is
+  // requested into the same stage.  The body has no branch: a branch would
+  // keep the scheduler from placing the copies and the fragment reads between
+  // the MFMAs.
+  auto kstep = [&](int cur_stage, const Tile& ct, IDX_T ck) {
     constexpr int S = BK / KB;
-    const int cur = kt % NSTAGES;
-    const elem_t* la = lds + cur * STAGE;
-    const elem_t* lb = la + A_STAGE;
-    const elem_t* na = lds + ((kt + 1) % NSTAGES) * STAGE;
+    const elem_t* la = lds + cur_stage * STAGE;
+    const elem_t* na = lds + ((cur_stage + 1) % NSTAGES) * STAGE;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
       FRAG_WAIT();
       if (s == S - FRAG_DIST) {
-        // Every read of stage `cur` has been issued and has completed (the
-        // barrier waits for this wave's LDS reads).  Once tile kt+1 has landed
-        // (tiles requested after it may stay in flight) and all waves are
-        // here, stage `cur` is free for tile kt+NSTAGES and the fragments of
-        // step kt+1 can be read.
-        if constexpr (MORE) {
-          wait_tiles(NSTAGES - 2);
-        } else {
-          const IDX_T last = KT - 1;
-          wait_tiles(last > kt + 1 ? (int)(last - (kt + 1)) : 0);
-        }
-        // This wave's reads of stage `cur` must be complete before any wave
+        // Every read of stage `cur_stage` has been issued and has completed
+        // (the barrier waits for this wave's LDS reads).  Once the next step's
+        // copies have landed (those requested after it may stay in flight)
+        // and all waves are here, the stage is free for step g+NSTAGES and
+        // the fragments of step g+1 can be read.
+        wait_tiles(NSTAGES - 2);
+        // This wave's reads of the stage must be complete before any wave
         // copies into it (the barrier alone does not wait for LDS reads).
         __builtin_amdgcn_s_waitcnt(0xC07F);
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
       }
-      // Reads for substep t of this step, or of the next one past the end
-      // (after the last step those read a stage that is never used again: in
-      // bounds, and waited for below).
+      // Reads for substep t of this step, or of the next one past the end.
       const int t = s + FRAG_DIST;
       const elem_t* ra = t < S ? la : na;
       const int ts = t < S ? t : t - S;
 #if DMA_SPREAD
       if (s >= S - FRAG_DIST) {
-        // The copies of tile kt+NSTAGES go out between the rows of MFMAs, a
+        // The copies of step g+NSTAGES go out between the rows of MFMAs, a
         // share after each row, so the matrix pipe is never left idle while
         // the wave issues a burst of them; the fragment reads go out after
         // the first row, and the remaining rows cover their latency.
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-#pragma unroll
-          for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s % NFB][i], bf[s % NFB][j], acc[i][j]);
+        for (int i = 0; i < MFMA_ROWS; ++i) {
+          mfma_row(i, s % NFB);
           __builtin_amdgcn_sched_barrier(0);
-          constexpr int R = FRAG_DIST * MI;
-          const int r = (s - (S - FRAG_DIST)) * MI + i;
-          if constexpr (MORE) dload_part(kt + NSTAGES, cur, r * (A_NV + B_NV) / R, (r + 1) * (A_NV + B_NV) / R);
+          constexpr int R = DMA_ROWS;
+          const int r = (s - (S - FRAG_DIST)) * MFMA_ROWS + i;
+          if (r < R) dload_part(ct, ck, cur_stage, r * (A_NV + B_NV) / R, (r + 1) * (A_NV + B_NV) / R);
           if (i == 0) fload(ra, ra + A_STAGE, ts, ts % NFB);
           __builtin_amdgcn_sched_barrier(0);
         }
         continue;
       }
 #else
-      if constexpr (MORE) {
-        if (s == S - FRAG_DIST) dload(kt + NSTAGES, cur);
-      }
+      if (s == S - FRAG_DIST) dload_part(ct, ck, cur_stage, 0, A_NV + B_NV);
 #endif
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s % NFB][i], bf[s % NFB][j], acc[i][j]);
+      mfma_all(s % NFB);
       // The reads are placed between these MFMAs, never ahead of them: with
       // direct loads in flight the only wait the compiler can place before an
       // MFMA is one for every outstanding LDS read, so a read issued before
@@ -494,12 +559,47 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  IDX_T kt = 0;
-  for (; kt + NSTAGES < KT; ++kt) kstep(kt, lego_bool<true>{});
-  for (; kt < KT; ++kt) kstep(kt, lego_bool<false>{});
-  // The reads issued in the last step are dead; let them land before the
-  // registers they target are reused.
-  __builtin_amdgcn_s_waitcnt(0xC07F);
+  // The stage of the current tile's step 0 (the ring advances KT steps per
+  // tile).
+  IDX_T stage0 = 0;
+  for (;;) {
+    const IDX_T npid = pid + (IDX_T)gridDim.x;
+    const bool has_next = PERSIST && npid < ntiles;
+    // The last NSTAGES steps of a tile request the first steps of the next
+    // one; the workgroup's last tile requests its own first steps again
+    // (landing in stages nothing reads), which keeps every step alike.
+    const Tile nxt = tile_of(has_next ? npid : pid);
+    if constexpr (RING_UNROLL && KT % NSTAGES == 0) {
+      // Every tile starts on stage 0: with the loop unrolled over the ring,
+      // each step's stage is a constant and its fragment addresses are
+      // loop-invariant registers (1.6% on the 8192^3 bf16 GEMM; plans with
+      // two waves per SIMD lack the registers for them).
+      for (IDX_T kt = 0; kt < KT; kt += NSTAGES) {
+#pragma unroll
+        for (int p = 0; p < NSTAGES; ++p) {
+          const bool own = kt + p + NSTAGES < KT;
+          kstep(p, own ? cur : nxt, (kt + p + NSTAGES) % KT);
+        }
+      }
+    } else {
+      for (IDX_T kt = 0; kt < KT; ++kt) {
+        const bool own = kt + NSTAGES < KT;
+        kstep((int)((stage0 + kt) % NSTAGES), own ? cur : nxt, (kt + NSTAGES) % KT);
+      }
+    }
+    store_c(cur.tm, cur.tn);
+    if (!has_next) break;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) acc[i][j] = (acc_t){};
+    pid = npid;
+    cur = nxt;
+    stage0 = (stage0 + KT) % NSTAGES;
+  }
+  // The fragment reads and copies issued by the last step are not used; they
+  // complete before the workgroup ends and before their registers are reused.
+  __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_sched_barrier(0);
 #elif (PREFETCH == 2 || ROLLING) && BK / KB >= 2
   // Register-staged pipeline.  With one wave per SIMD (the accumulators
@@ -528,10 +628,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
       }
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      mfma_all(s & 1);
       if (s + 1 < S) fload(la, lb, s + 1, (s + 1) & 1);
       else if (kt + 1 < KT) {
         const elem_t* na = lds + (cur ^ 1) * STAGE;
@@ -587,10 +684,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       if (s + 1 < BK / KB) fload(la, lb, s + 1, (s + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);
       if (s == STORE_AT && kt + 1 < KT) sstore(cur ^ 1, 0);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j) acc[i][j] = MFMA(af[s & 1][i], bf[s & 1][j], acc[i][j]);
+      mfma_all(s & 1);
       if (s == STORE_AT) {
 #pragma unroll
         for (int g = 0; g < A_NV * (A_SVEC ? A_VR : A_V) + B_NV * (B_SVEC ? B_VR : B_V); ++g) {
@@ -603,23 +697,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     __syncthreads();
   }
 #endif
-
-#if C_SEP
-  float* __restrict__ Cb = C + c_t(tm, tn);
+#if !DIRECT_LDS
+  store_c(tm, tn);
 #endif
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NI; ++j)
-#pragma unroll
-      for (int r = 0; r < NREG; ++r) {
-#if C_EDGE
-        if (!c_ok(tm, tn, lane, w, i, j, r)) continue;
-#endif
-#if C_SEP
-        __builtin_nontemporal_store(acc[i][j][r], Cb + c_l(lane, w, i, j, r));
-#else
-        __builtin_nontemporal_store(acc[i][j][r], C + c_f(tm, tn, lane, w, i, j, r));
-#endif
-      }
 }

@@ -21,10 +21,12 @@ struct FnCache {
   FnCache& operator=(const FnCache&) {
     std::lock_guard<std::mutex> lk(mu);
     for (auto& f : fn) f = nullptr;
+    for (auto& r : resident) r = 0;
     return *this;
   }
   mutable std::mutex mu;
   mutable void* fn[kDevices] = {};
+  mutable long long resident[kDevices] = {};  // workgroups resident at once (persistent plans)
 };
 
 struct KernelPlan {
@@ -33,6 +35,8 @@ struct KernelPlan {
   long long grid = 1;   // workgroups (1D)
   int block = 256;      // threads per workgroup
   std::string info;     // human-readable summary (path, vector widths, op counts)
+  bool persistent = false;  // the kernel walks tiles grid-stride: launch at most
+                            // as many workgroups as fit on the device at once
   FnCache fns;          // filled by the first launch on each device
 };
 

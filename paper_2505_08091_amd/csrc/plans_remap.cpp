@@ -7,6 +7,7 @@
 #include "errors.hpp"
 #include "lower.hpp"
 #include "plans.hpp"
+#include "tune.hpp"
 
 namespace lego {
 
@@ -69,9 +70,9 @@ KernelPlan plan_index_eval(const Layout& l, int which, int idx_bytes) {
   // 8192^2 maps, the speed of a plain fill, against 5.2 TB/s with streaming
   // stores from a 16384-workgroup grid-stride loop.
   int nt_store = 0;
-  if (const char* e = std::getenv("LEGO_INDEX_NT")) nt_store = std::atoi(e) != 0;
+  nt_store = tune("index.nt_store", nt_store) != 0;
   long long max_grid = 1ll << 24;
-  if (const char* e = std::getenv("LEGO_INDEX_GRID")) max_grid = std::max(1ll, std::atoll(e));
+  max_grid = std::max(1ll, (long long)tune("index.grid", max_grid));
   std::ostringstream s;
   s << header() << "#define NT_STORE " << nt_store << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define OUT_T "
     << (idx_bytes == 4 ? "int" : "long long") << "\n#define PPT " << 16 / idx_bytes << "\n#define RANK "
@@ -292,7 +293,7 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
                               {"bdst", addr_fn(&dst)}},
                              &wide, &info);
   int nontemporal = 0;
-  if (const char* e = std::getenv("LEGO_REMAP_NONTEMPORAL")) nontemporal = std::atoi(e);
+  nontemporal = (int)tune("remap.nontemporal", nontemporal);
   std::ostringstream s;
   s << header() << "#define ELEM_T " << elem_type(elem_bytes) << "\n#define IDX_T " << (wide ? "i64" : "u32")
     << "\n#define BR " << B << "\n#define BC " << B << "\n#define BPAD " << pad << "\n#define NBR " << nbr << "\n#define NBC " << nbc
@@ -378,7 +379,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   if (R.path == REMAP_GATHER && !masked && !dst.expand_inner && N == NS) {
     RemapPlan box;
     bool use = plan_remap_box(src, dst, elem_bytes, &box);
-    if (const char* e = std::getenv("LEGO_REMAP_BOX")) use = use && std::atoi(e) != 0;
+    use = use && tune("remap.box", 1) != 0;
     if (use) return box;
   }
 
@@ -393,14 +394,14 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   // times over neighbouring chunks, so its loads stay cached (Row <->
   // antidiagonal 4096^2 fp32: 0.74/0.97 -> 1.11/1.78 TB/s).
   int nontemporal = R.path == REMAP_GATHER ? 0 : 1;
-  if (const char* e = std::getenv("LEGO_REMAP_NONTEMPORAL")) nontemporal = std::atoi(e);
+  nontemporal = (int)tune("remap.nontemporal", nontemporal);
   if (R.path == REMAP_DIRECT || R.path == REMAP_GATHER) {
     // 8 vectors in flight per thread (a 32 KiB chunk per workgroup at 16-byte
     // vectors): measured ahead of 2, 4 and 16, and of 128/512/1024 threads.
     int NT = 256, UNROLL = 8;
-    if (const char* e = std::getenv("LEGO_REMAP_NT")) NT = std::atoi(e);
-    const char* unroll_env = std::getenv("LEGO_REMAP_UNROLL");
-    if (unroll_env) UNROLL = std::atoi(unroll_env);
+    NT = (int)tune("remap.nt", NT);
+    const bool unroll_set = tune("remap.unroll", 0) != 0;
+    UNROLL = (int)tune("remap.unroll", UNROLL);
     const i64 nvec = N / V;
     // Source vector of destination vector t, as an expression of t.
     auto src_vec_of = [&](Ctx& c, const Sum& t) {
@@ -416,7 +417,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     bool src_sep = false;
     if (!pure) {
       for (int u : {8, 4, 2, 1}) {
-        if (unroll_env && u != UNROLL) continue;
+        if (unroll_set && u != UNROLL) continue;
         const i64 ch = (i64)NT * u;
         if (nvec % ch) continue;
         Ctx c;
@@ -436,7 +437,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     // otherwise they run in destination order.
     std::vector<Dg> cd;  // digits of the chunk index: (dst weight in chunks, size, src weight)
     bool src_order = pure && nvec % chunk == 0;
-    if (const char* e = std::getenv("LEGO_REMAP_ORDER")) src_order = src_order && std::string(e) != "dst";
+    src_order = src_order && tune("remap.order", 1) != 0;
     if (src_order) {
       std::vector<Dg> d;
       for (auto& x : digits) d.push_back({x.a, x.b, x.coeff});
@@ -464,7 +465,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     // (Measured on the element-gather path: Row <-> antidiagonal 4096^2 fp32
     // 0.42/0.63 -> 0.74/0.98 TB/s; vector maps gain nothing from it.)
     bool xcd_blocks = !src_order && !pure && nblk % 8 == 0 && R.path == REMAP_GATHER;
-    if (const char* e = std::getenv("LEGO_REMAP_XCD")) xcd_blocks = xcd_blocks && std::atoi(e) != 0;
+    xcd_blocks = xcd_blocks && tune("remap.xcd", 1) != 0;
     std::vector<std::pair<std::string, std::function<FnSpec(Ctx&)>>> dfns = {{"blk",
                                  [&](Ctx& c) {
                                    int b = c.var("b", nblk);
@@ -531,7 +532,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     R.block = NT;
     // Optionally a persistent grid: `persist` workgroups per CU loop over the chunks.
     int persist = 0;
-    if (const char* e = std::getenv("LEGO_REMAP_PERSIST")) persist = std::atoi(e);
+    persist = (int)tune("remap.persist", persist);
     R.grid = persist > 0 ? std::min<i64>(nblk, 256ll * persist) : nblk;
     R.vec = V;
     R.vec_dst = V;
@@ -560,7 +561,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   const bool hbm_bound =
       2 * N * elem_bytes > (256ll << 20) || (run == 1 && N * elem_bytes >= 1024ll * 64 * 1024);
   i64 tile_bytes = hbm_bound ? (run == 1 ? 64 * 1024 : 32 * 1024) : 16 * 1024;
-  if (const char* e = std::getenv("LEGO_REMAP_TILE_BYTES")) tile_bytes = std::max<i64>(256, std::atoll(e));
+  tile_bytes = std::max<i64>(256, tune("remap.tile_bytes", tile_bytes));
   const i64 max_tile = std::min<i64>(N, std::max<i64>(32 * 1024, tile_bytes) / elem_bytes);
   i64 tdst = std::min<i64>(N, std::max<i64>(maxv, 256 / elem_bytes));
   i64 tsrc = std::min<i64>(N, std::max<i64>(maxv, 256 / elem_bytes));
@@ -588,7 +589,7 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   // Tile order (the digit layout over tiles): source order for HBM-bound
   // remaps, destination order otherwise.
   bool lds_src_order = hbm_bound;
-  if (const char* e = std::getenv("LEGO_REMAP_ORDER")) lds_src_order = std::string(e) == "src";
+  lds_src_order = tune("remap.order", lds_src_order) != 0;
   if (lds_src_order) std::sort(gd.begin(), gd.end(), [&](size_t x, size_t y) { return d[x].c < d[y].c; });
   ts = td;
   std::sort(ts.begin(), ts.end(), [&](size_t x, size_t y) { return d[x].c < d[y].c; });

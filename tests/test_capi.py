@@ -60,6 +60,16 @@ def test_version_and_last_error(lego):
     (lambda L: L.gemm_plan(64, 64, 64, "f16", a=L.ExpandBy([60, 64], [64, 64], L.as_layout(L.Row(64, 64)))),
      "UNSUPPORTED"),
     (lambda L: L.mfma_fragment_layout(7, 0), "INVALID_ARG"),
+    # TileOrderBy levels must all have rank d; GroupBy tile levels equal rank
+    (lambda L: L._tileorderby_d(2, L.Row(4, 4), L.Row(2, 2, 2)), "INVALID_ARG"),
+    (lambda L: L._tileorderby_d(3, L.Row(4, 4), L.Row(2, 2)), "INVALID_ARG"),
+    (lambda L: L.GroupByTiles([4, 4], [2, 0]), "INVALID_ARG"),
+    # LDS stages: 3 x 64 KiB of a 256x256x64 tile exceed the 160 KiB LDS; 1 is
+    # no ring; a register-staged plan (A in 2x4 blocks) has exactly two
+    (lambda L: L.gemm_plan(1024, 1024, 1024, "bf16", stages=3), "UNSUPPORTED"),
+    (lambda L: L.gemm_plan(1024, 1024, 1024, "bf16", stages=1), "UNSUPPORTED"),
+    (lambda L: L.gemm_plan(1024, 1024, 1024, "bf16", stages=3, a=L.TileOrderBy(L.Row(512, 256), L.Row(2, 4))),
+     "UNSUPPORTED"),
 ])
 def test_error_codes(lego, call, status):
     with pytest.raises(lego.LegoError) as e:
@@ -323,3 +333,24 @@ def test_index_map_output_alignment_checked(lego):
     lay = lego.as_layout(lego.Row(8, 8))
     for f in (lego._lib.lego_apply_all_device, lego._lib.lego_inv_all_device):
         assert f(lay.h, 4, ctypes.c_void_p((1 << 20) + 4), None) == -1
+
+
+def test_groupby_tiles_is_the_concatenated_logical_view(lego):
+    """GroupBy over tile levels (Figure 3) has the levels' coordinates as its
+    logical index: the same layout as a GroupBy over their concatenation, and
+    chained with the same OrderBy it maps every point alike (Figure 6)."""
+    g1 = lego.GroupByTiles([2, 3], [2, 3]).OrderBy(lego.RegP([2, 3, 2, 3], [1, 3, 2, 4]))
+    g2 = lego.GroupBy([2, 3], [2, 3]).OrderBy(lego.RegP([2, 3, 2, 3], [1, 3, 2, 4]))
+    o = OL.GroupBy([2, 3, 2, 3]).OrderBy(OL.RegP([2, 3, 2, 3], [1, 3, 2, 4]))
+    assert g1.dims() == [2, 3, 2, 3]
+    for x in range(36):
+        idx = [int(v) for v in OL.canon_unflatten([2, 3, 2, 3], x)]
+        assert g1.apply(idx) == g2.apply(idx) == int(o.apply(idx))
+
+
+def test_gemm_stages_field(lego):
+    """The descriptor's LDS stage count: 4 stages of a 256x256x32 tile fit
+    (4 x 32 KiB); the plan reports what it uses, and 0 lets the planner choose."""
+    assert " stages 4 " in lego.gemm_plan(1024, 1024, 1024, "bf16", bk=32, stages=4)
+    assert " stages 2 " in lego.gemm_plan(1024, 1024, 1024, "bf16", bk=32, stages=2)
+    assert " stages 2 " in lego.gemm_plan(1024, 1024, 1024, "bf16")

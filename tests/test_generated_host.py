@@ -336,6 +336,7 @@ int main() {
           u64 o = (u64)c_f((IDX_T)tm, (IDX_T)tn, (IDX_T)lane, (IDX_T)w, (IDX_T)mi, (IDX_T)ni, (IDX_T)r);
 #endif
           if (o >= GEMM_M * GEMM_N || c[o]++) FAIL("C offset bad");
+
         }
   }
   printf("ok\n");
@@ -380,12 +381,16 @@ def _compile_and_run(src, harness, tmp, args=()):
     return r.stdout
 
 
-@pytest.mark.parametrize("i", range(11))
+N_SOURCES = 13
+
+
+def test_source_count():
+    assert len(_sources()) == N_SOURCES
+
+
+@pytest.mark.parametrize("i", range(N_SOURCES))
 def test_generated_source_on_host(i):
-    srcs = _sources()
-    if i >= len(srcs):
-        pytest.skip("no such source")
-    name, src = srcs[i]
+    name, src = _sources()[i]
     assert MARK in src
     with tempfile.TemporaryDirectory() as tmp:
         out = os.path.join(tmp, "out.bin")
@@ -438,7 +443,7 @@ def _remap_cases():
     from tests.test_gpu_genexpr import _expr_cases
     from tests.test_gpu_remap import _expand_cases, _small_cases
     cases = [(n, ls, ld, ols, old) for n, ls, ld, ols, old in _small_cases(L) + _expand_cases(L) + _expr_cases(L)]
-    for n in (2048, 4096, 1024):
+    for n in (2048, 4096, 8192, 1024):
         cases.append((f"transpose {n}", L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n)),
                       OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.Col(n, n))))
     cases.append(("identity 8192", L.as_layout(L.Row(8192, 8192)), L.as_layout(L.Row(8192, 8192)),
@@ -504,6 +509,10 @@ def _gemm_cases():
     for la, lb in (("Row", "Row"), ("Col", "Row"), ("Col", "Col")):  # m/n-contiguous operands, default plan
         cases.append(dict(M=2048, N=2048, K=2048, dtype="f16", a=L.as_layout(getattr(L, la)(2048, 2048)),
                           b=L.as_layout(getattr(L, lb)(2048, 2048))))
+    for la in ("Row", "Col"):  # the four operand variants at 4096^3, default plan
+        for lb in ("Row", "Col"):
+            cases.append(dict(M=4096, N=4096, K=4096, dtype="f16", a=L.as_layout(getattr(L, la)(4096, 4096)),
+                              b=L.as_layout(getattr(L, lb)(4096, 4096))))
     from tests.test_gpu_gemm import _ragged_cases
     cases += [{k: v for k, v in c.items() if k not in ("oa", "ob")} for c in _ragged_cases(L)]
     from tests.test_gpu_gemm import _sched_cases
@@ -512,19 +521,70 @@ def _gemm_cases():
     from tests import genp_exprs as GE
     sw = L.as_layout(L.GenPExpr([256, 64], GE.SWIZZLE64_APPLY, GE.SWIZZLE64_INV))
     cases.append(dict(M=1024, N=1024, K=1024, dtype="bf16", lds_a=sw, lds_b=sw))
+    from tests.test_gpu_gemm import _persistent_cases
+    cases += [{k: v for k, v in c.items() if k not in ("oa", "ob", "max_workgroups")} for c in _persistent_cases(L)]
     return cases
 
 
-@pytest.mark.parametrize("i", range(34))
+N_GEMM_CASES = 42
+
+
+def test_gemm_case_count():
+    assert len(_gemm_cases()) == N_GEMM_CASES
+
+
+@pytest.mark.parametrize("i", range(N_GEMM_CASES))
 def test_gemm_sources_of_gpu_cases(i):
     import paper_2505_08091_amd as L
-    cases = _gemm_cases()
-    if i >= len(cases):
-        pytest.skip("no such case")
-    kw = cases[i]
+    kw = _gemm_cases()[i]
     src = L.plan_source("gemm", **kw)
     with tempfile.TemporaryDirectory() as tmp:
         assert _compile_and_run(src, HARNESS_GEMM, tmp).strip() == "ok", kw
+
+
+HARNESS_ISQRT32_ALL = r"""
+#include <omp.h>
+int main() {
+  // every 32-bit operand: r = floor(sqrt(v)) exactly
+  unsigned long long bad = 0;
+#pragma omp parallel for reduction(+ : bad) schedule(static)
+  for (long long hi = 0; hi < 65536; ++hi)
+    for (u64 lo = 0; lo < 65536; ++lo) {
+      const u64 v = ((u64)hi << 16) | lo;
+      const u64 r = lego_isqrt((u32)v);
+      bad += !(r * r <= v && (r + 1) * (r + 1) > v);
+    }
+  printf("%llu\n", bad);
+  return bad != 0;
+}
+"""
+
+
+@pytest.mark.parametrize("estimate", ["float", "perturbed"])
+def test_integer_square_root_32bit_exhaustive(estimate):
+    """The 32-bit integer square root of the generated code on all 2^32
+    operands.  It starts from a float square-root estimate and corrects it by
+    integer comparisons; the second case replaces the estimate by one that is
+    off by -2..+1 (a pseudo-random offset per operand), so exactness does not
+    rest on how the device rounds its square root."""
+    import paper_2505_08091_amd as L
+    src = L.plan_source("apply", L.as_layout(L.GenP("antidiag", [64, 64])), param=4)
+    head = src.split(MARK)[0]
+    if estimate == "perturbed":
+        head = ("static inline float lego_bad_sqrt(float x) {\n"
+                "  const unsigned v = (unsigned)x;\n"
+                "  const float s = __builtin_sqrtf(x) + (float)((int)((v * 2654435761u) >> 30) - 2);\n"
+                "  return s < 0.f ? 0.f : s;\n"
+                "}\n#define __builtin_sqrtf(x) lego_bad_sqrt(x)\n") + head
+    with tempfile.TemporaryDirectory() as tmp:
+        cpp, exe = os.path.join(tmp, "s.cpp"), os.path.join(tmp, "s")
+        with open(cpp, "w") as f:
+            f.write(HARNESS_COMMON + head + HARNESS_ISQRT32_ALL)
+        r = subprocess.run(["g++", "-O2", "-std=c++17", "-fopenmp", "-w", cpp, "-o", exe], capture_output=True,
+                           text=True)
+        assert r.returncode == 0, r.stderr[-4000:]
+        r = subprocess.run([exe], capture_output=True, text=True, timeout=600)
+        assert r.returncode == 0 and r.stdout.strip() == "0", (r.stdout, r.stderr)
 
 
 HARNESS_ISQRT = r"""

@@ -51,15 +51,25 @@ def test_remap_c5_row_morton_roundtrip(lego):
     assert (bits(back) == bits(src)).all()
 
 
-@pytest.mark.parametrize("n,dtype", [(2048, "f32"), (4096, "f16"), (1024, "bf16")])
+@pytest.mark.parametrize("n,dtype", [(2048, "f32"), (4096, "f32"), (8192, "f32"), (4096, "f16"), (1024, "bf16")])
 def test_remap_transpose(lego, n, dtype):
-    """Row -> Col (the transpose of Table V) equals a numpy transpose."""
+    """Row -> Col and Col -> Row (the transpose of Table V), each direction on
+    its own source, every element against the oracle's remap.  The fp32
+    sizes are the measured ones; 4096^2 and 8192^2 take the 64 KiB tiles read
+    in source order, which the plan text must show."""
     dev = need_gpu()
-    src = S.tensor(n * n, dtype, seed=S.SEED_SRC)
     row, col = lego.as_layout(lego.Row(n, n)), lego.as_layout(lego.Col(n, n))
-    say(f"remap transpose n={n} {dtype} plan={lego.remap_plan(row, col, src.element_size())['info']}")
-    out = _run(lego, row, col, src, dev)
-    assert (bits(out) == bits(src).reshape(n, n).T.ravel()).all()
+    orow, ocol = OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.Col(n, n))
+    for seed, (ls, ld, ols, old, name) in enumerate(((row, col, orow, ocol, "row->col"),
+                                                     (col, row, ocol, orow, "col->row"))):
+        src = S.tensor(n * n, dtype, seed=S.SEED_SRC + seed)
+        info = lego.remap_plan(ls, ld, src.element_size())["info"]
+        say(f"remap transpose {name} n={n} {dtype} plan={info}")
+        if dtype == "f32" and n >= 4096:
+            assert info.startswith("lds TILE=16384 ") and " src-order " in info, info
+        out = _run(lego, ls, ld, src, dev)
+        exp = OR.remap(ols, old, bits(src))
+        assert (bits(out) == exp).all(), name
 
 
 @pytest.mark.parametrize("b", [8, 4])
