@@ -801,7 +801,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // Loop unrolled over the LDS ring when one wave per SIMD leaves the
   // registers for per-stage fragment addresses.
   const int ring_unroll = (int)tune("gemm.ring_unroll", MI * NI * NREG > 128 ? 1 : 0);
-  s << "#define RING_UNROLL " << ring_unroll << "\n";
+  s << "#define RING_UNROLL " << ring_unroll << "\n#define FRAG_SPREAD " << tune("gemm.frag_spread", 2) << "\n";
   s << "#define PREFETCH " << prefetch << "\n#define ROLLING " << rolling << "\n#define DMA_SPREAD " << dma_spread
     << "\n#define FRAG_DIST " << frag_dist << "\n#define DIRECT_LDS " << (direct ? 1 : 0)
     << "\n#define NSTAGES " << nstages << "\n";

@@ -116,6 +116,9 @@ LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
 #endif
 // MFMA rows after the stage barrier over which the copies of a step are
 // spread.
+#ifndef FRAG_SPREAD
+#define FRAG_SPREAD 0
+#endif
 #ifndef DMA_ROWS
 #define DMA_ROWS (FRAG_DIST * MFMA_ROWS)
 #endif
@@ -291,9 +294,12 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // Fragments of one k-substep, double-buffered in registers: the reads of
   // substep s+1 are in flight while the MFMAs of substep s run.
   mf_t af[NFB][MI], bf[NFB][NI];
-  auto fload = [&](const elem_t* la, const elem_t* lb, int s, int buf) {
+  // Fragments [lo, hi) of substep s into set buf: A's MI fragments, then
+  // B's NI.
+  auto fload_part = [&](const elem_t* la, const elem_t* lb, int s, int buf, int lo, int hi) {
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
+      if (i < lo || i >= hi) continue;
 #if A_FRTR
       af[buf][i] = lds_frag_tr(la, a_ft(lane, w, i, s, 0), a_ft(lane, w, i, s, 1));
 #elif A_FRVEC
@@ -307,6 +313,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     }
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
+      if (MI + j < lo || MI + j >= hi) continue;
 #if B_FRTR
       bf[buf][j] = lds_frag_tr(lb, b_ft(lane, w, j, s, 0), b_ft(lane, w, j, s, 1));
 #elif B_FRVEC
@@ -319,6 +326,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #endif
     }
   };
+  auto fload = [&](const elem_t* la, const elem_t* lb, int s, int buf) { fload_part(la, lb, s, buf, 0, MI + NI); };
 
   // Row r of the MFMAs of one substep with fragment set fb: every MFMA of a
   // row has the same first operand, A's fragment r.
@@ -530,18 +538,63 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         // the first row, and the remaining rows cover their latency.
 #pragma unroll
         for (int i = 0; i < MFMA_ROWS; ++i) {
-          mfma_row(i, s % NFB);
-          __builtin_amdgcn_sched_barrier(0);
           constexpr int R = DMA_ROWS;
           const int r = (s - (S - FRAG_DIST)) * MFMA_ROWS + i;
+#if FRAG_SPREAD
+          // Each row: its MFMAs with this row's share of the copies and of
+          // the next fragments between them, one instruction after each MFMA.
+          mfma_row(i, s % NFB);
+          if (r < R) dload_part(ct, ck, cur_stage, r * (A_NV + B_NV) / R, (r + 1) * (A_NV + B_NV) / R);
+          fload_part(ra, ra + A_STAGE, ts, ts % NFB, i * (MI + NI) / MI, (i + 1) * (MI + NI) / MI);
+          // after MFMA g of the row: a copy (even g) or a fragment read (odd
+          // g); with FRAG_SPREAD 3 the copy's LDS address (M0) is set one
+          // MFMA ahead, so no wait state separates the two
+#pragma unroll
+          for (int g = 0; g < NI; ++g) {
+            if (FRAG_SPREAD >= 3 && g % 2 == 0 && g / 2 < (A_NV + B_NV) / R)
+              __builtin_amdgcn_sched_group_barrier(0x004, 1, 0);  // M0
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            if (g % 2 == 0 && g / 2 < (A_NV + B_NV) / R) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            if (g % 2 == 1 && g / 2 < (MI + NI) / MI) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#else
+          mfma_row(i, s % NFB);
+          __builtin_amdgcn_sched_barrier(0);
           if (r < R) dload_part(ct, ck, cur_stage, r * (A_NV + B_NV) / R, (r + 1) * (A_NV + B_NV) / R);
           if (i == 0) fload(ra, ra + A_STAGE, ts, ts % NFB);
           __builtin_amdgcn_sched_barrier(0);
+#endif
         }
         continue;
       }
 #else
       if (s == S - FRAG_DIST) dload_part(ct, ck, cur_stage, 0, A_NV + B_NV);
+#endif
+#if FRAG_SPREAD >= 2
+      // The next fragments go out one after each MFMA of the first rows, so
+      // that the last is issued well before the substep ends (the substep
+      // before the stage barrier waits for all of them).
+      {
+        // FR reads over the first ROWS rows (one per MFMA where the rows have
+        // enough MFMAs; the rows present take them all otherwise).
+        constexpr int FR = MI + NI;
+        constexpr int ROWS = (FR + NI - 1) / NI < MFMA_ROWS ? (FR + NI - 1) / NI : MFMA_ROWS;
+#pragma unroll
+        for (int i = 0; i < MFMA_ROWS; ++i) {
+          mfma_row(i, s % NFB);
+          if (i < ROWS) {
+            fload_part(ra, ra + A_STAGE, ts, ts % NFB, i * FR / ROWS, (i + 1) * FR / ROWS);
+#pragma unroll
+            for (int g = 0; g < NI; ++g) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      continue;
 #endif
       mfma_all(s % NFB);
       // The reads are placed between these MFMAs, never ahead of them: with
