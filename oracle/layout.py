@@ -29,8 +29,9 @@ test in ``tests/test_oracle_pins.py``):
   coordinates go to tile-major storage, level h ordered by P^h.  The printed
   definition is garbled.
 * Figure 2's p^{-1} (not shown in the paper) is B^{-1}([n1,n2], n1*n2-1-x).
-* The antidiagonal code of Figure 7 uses exact integer division (the operands
-  are even) and the exact integer square root.
+* The antidiagonal order of Figure 7 is taken from what it computes: the
+  antidiagonals in turn, rows increasing within one (the printed code's real
+  division and square root are not needed to count that way).
 * Morton (Z) order puts column bits at even and row bits at odd positions, so
   every 2x2 block reads 0,1,2,3 in row-major order.
 * The XOR swizzle over [R, C] with vector width v and row divisor s is
@@ -309,38 +310,32 @@ def reverse_genp(n1, n2):
     return GenP([n1, n2], f, finv, name="reverse")
 
 
-def _isqrt(x):
-    if isinstance(x, np.ndarray):
-        return np.array([math.isqrt(int(v)) for v in x.ravel()], dtype=np.int64).reshape(x.shape)
-    return math.isqrt(int(x))
-
-
-def _where(c, a, b):
-    if isinstance(c, np.ndarray):
-        return np.where(c, a, b)
-    return a if c else b
+def _antidiag_starts(n):
+    """start[d] for d = 0..2n-1: the number of points on the antidiagonals
+    before antidiagonal d of an n x n tile (antidiagonal d, i + j = d, holds
+    min(d + 1, 2n - 1 - d) points)."""
+    d = np.arange(2 * n - 1, dtype=np.int64)
+    return np.concatenate([[0], np.cumsum(np.minimum(d + 1, 2 * n - 1 - d))])
 
 
 def antidiag(n, i, j):
-    """Antidiagonal order of an n x n tile (Figure 7): elements are numbered in
-    the order of the 2n-1 antidiagonals, top row first within an antidiagonal."""
-    a = i + j + 1
-    first = i + (a * (a - 1)) // 2
-    b = 2 * n - a
-    second = n * n - n + i - (b * (b - 1)) // 2
-    return _where(a <= n, first, second)
+    """Antidiagonal order of an n x n tile (Figure 7): the elements are
+    numbered antidiagonal by antidiagonal (i + j ascending) and, within one,
+    by increasing row.  The number of (i, j) is the count of the points on the
+    earlier antidiagonals plus the points of its own antidiagonal with a
+    smaller row (the rows of antidiagonal d start at max(0, d - n + 1))."""
+    d = np.asarray(i) + np.asarray(j)
+    return _antidiag_starts(n)[d] + i - np.maximum(0, d - n + 1)
 
 
-def antidiag_inv(n, x0):
-    """Inverse of :func:`antidiag` (Figure 7) with the exact integer sqrt."""
-    s = n * (n + 1) // 2
-    upper = x0 < s
-    x = _where(upper, x0, n * n - 1 - x0)
-    a = _isqrt(2 * x)
-    a = a + _where(x >= (a * (a + 1)) // 2, 1, 0)
-    i = x - (a * (a - 1)) // 2
-    j = a - i - 1
-    return [_where(upper, i, n - 1 - i), _where(upper, j, n - 1 - j)]
+def antidiag_inv(n, x):
+    """Inverse of :func:`antidiag`: the antidiagonal whose block of numbers
+    holds x (a search in the cumulative counts), then the row from the offset
+    of x within it."""
+    start = _antidiag_starts(n)
+    d = np.searchsorted(start, x, side="right") - 1
+    i = x - start[d] + np.maximum(0, d - n + 1)
+    return [i, d - i]
 
 
 def antidiag_genp(n):

@@ -277,13 +277,18 @@ typename A::V Piece::genp_apply(const A& al, const std::vector<typename A::V>& i
       // [0, size), and it tells the lowering the range of the result.
       return al.mod(eval_gexpr(al, *ex->apply, i), size());
     case GEN_ANTIDIAG: {
-      // Figure 7: order of the 2n-1 antidiagonals, top row first.
+      // Figure 7's order: the antidiagonals d = i + j in turn, rows
+      // increasing within one.  On the upper triangle (d < n) the points
+      // before (i, j) are the d(d+1)/2 of the earlier antidiagonals and the i
+      // above it on its own; the lower triangle is the upper one turned by
+      // 180 degrees: n*n - 1 minus the number of the turned point
+      // (n-1-i, n-1-j), which lies on antidiagonal 2n-2-d.
       i64 nn = n[0];
-      V a = al.add(al.add(i[0], i[1]), al.c(1));
-      V first = al.add(i[0], al.div(al.mul(a, al.sub(a, al.c(1))), 2));
-      V b = al.sub(al.c(2 * nn), a);
-      V second = al.sub(al.add(al.c(nn * nn - nn), i[0]), al.div(al.mul(b, al.sub(b, al.c(1))), 2));
-      return al.sel(al.lt(a, al.c(nn + 1)), first, second);
+      V d = al.add(i[0], i[1]);
+      V up = al.add(al.div(al.mul(d, al.add(d, al.c(1))), 2), i[0]);
+      V e = al.sub(al.c(2 * nn - 2), d);
+      V turned = al.add(al.div(al.mul(e, al.add(e, al.c(1))), 2), al.sub(al.c(nn - 1), i[0]));
+      return al.sel(al.lt(d, al.c(nn)), up, al.sub(al.c(nn * nn - 1), turned));
     }
   }
   throw std::logic_error("unknown GenP");

@@ -104,6 +104,22 @@ def test_antidiag_bijection_and_inverse(n):
     assert (np.diff(s) >= 0).all()
 
 
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 12])
+def test_antidiag_equals_brute_force_ranking(n):
+    """Figure 7's order by brute force: rank every (i, j) of the tile by
+    (antidiagonal i + j, then row i); the rank is the number."""
+    pts = sorted(((i + j, i), (i, j)) for i in range(n) for j in range(n))
+    for rank, (_, (i, j)) in enumerate(pts):
+        assert int(L.antidiag(n, i, j)) == rank
+        assert [int(v) for v in L.antidiag_inv(n, rank)] == [i, j]
+
+
+def test_antidiag_figure6_value():
+    """Figure 6's walk-through lands on 15 = block 1, element 6: element (1, 2)
+    of a 3 x 3 block in antidiagonal order is 6."""
+    assert int(L.antidiag(3, 1, 2)) == 6
+
+
 # ------------------------------------------------------------ Table I rows
 @pytest.mark.parametrize("M,K,BM,BK", [(8, 12, 4, 3), (16, 8, 4, 4), (6, 10, 3, 5)])
 def test_table1_tileby_row_is_cute_strides(M, K, BM, BK):
