@@ -385,9 +385,34 @@ Sum lt(const Ctx& c, const Sum& x, const Sum& y) {
 }
 
 Sum select(const Ctx& c, const Sum& cond, const Sum& x, const Sum& y) {
-  (void)c;
   if (cond.is_const()) return cond.c0 ? x : y;
   if (skey(x) == skey(y)) return x;
+  // Terms both operands have, with equal coefficients, are added outside:
+  // c ? X + t : Y + t = t + (c ? X : Y).  (A term of a variable common to
+  // both branches then stays out of the select, so a sum can still be split
+  // by that variable.)
+  Sum common, xr, yr;
+  xr.c0 = x.c0;
+  yr.c0 = y.c0;
+  size_t i = 0, j = 0;
+  while (i < x.t.size() || j < y.t.size()) {
+    const int cmp = i == x.t.size() ? 1 : j == y.t.size() ? -1 : x.t[i].a->key.compare(y.t[j].a->key);
+    if (cmp < 0) {
+      xr.t.push_back(x.t[i++]);
+    } else if (cmp > 0) {
+      yr.t.push_back(y.t[j++]);
+    } else {
+      if (x.t[i].c == y.t[j].c) {
+        common.t.push_back(x.t[i]);
+      } else {
+        xr.t.push_back(x.t[i]);
+        yr.t.push_back(y.t[j]);
+      }
+      ++i;
+      ++j;
+    }
+  }
+  if (!common.t.empty()) return add(c, common, select(c, cond, xr, yr));
   Interval rx = range(x), ry = range(y);
   return atom_sum(make_op(Op::Select, {cond, x, y}, 0, {std::min(rx.lo, ry.lo), std::max(rx.hi, ry.hi)}));
 }

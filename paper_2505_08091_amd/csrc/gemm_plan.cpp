@@ -894,6 +894,11 @@ std::vector<std::pair<std::string, std::string>> selftest_sources() {
   out.push_back({"remap morton->row f16", plan_remap(*mz, *r4, 2).src});
   LayoutP col = make_from_piece(make_col({8192, 8192}));
   out.push_back({"remap row->col f32", plan_remap(*row, *col, 4).src});
+  // Row <-> antidiagonal order of 4096^2 fp32 (the box path).
+  LayoutP ad = make_from_piece(make_genp(GEN_ANTIDIAG, {4096, 4096}, {}));
+  LayoutP r4f = make_from_piece(make_row({4096, 4096}));
+  out.push_back({"remap row->antidiag f32", plan_remap(*r4f, *ad, 4).src});
+  out.push_back({"remap antidiag->row f32", plan_remap(*ad, *r4f, 4).src});
   // GEMMs.
   GemmRequest g1;
   g1.M = g1.N = g1.K = 128;

@@ -18,14 +18,18 @@
 //   LEGO_FN IDX_T ldsw(IDX_T q, IDX_T e)      LDS slot of element e of that vector
 //   LEGO_FN IDX_T ldsr(IDX_T q)               LDS slot of destination-side vector q
 //   LEGO_FN IDX_T dst_off(IDX_T g, IDX_T q)   element offset of destination-side vector q
-// Box path (2-D maps without digit structure): a BR x BC box of the logical
-// index space is read in one order and written in another, through LDS:
-//   BR, BC, BPAD, NBR x NBC (the grid of boxes), EXT0, EXT1 (logical extents), NT
+// Box path (2-D maps without digit structure): a BX x BX box of the logical
+// index space is read line by line in one kind of line and written in another,
+// through LDS:
+//   BX, BPAD, NBR x NBC (the grid of boxes), EXT0, EXT1 (logical extents), NT
+//   S_ORD, D_ORD     kind of line of the load and store sides (0 rows, 1
+//                    columns, 2 pairs of antidiagonals of the box)
 //   LEGO_FN void bord(IDX_T b, IDX_T* bi, IDX_T* bj)  box of workgroup b
-//   LEGO_FN void ws(IDX_T q, IDX_T* a, IDX_T* b)   box element read q-th
-//   LEGO_FN void wd(IDX_T q, IDX_T* a, IDX_T* b)   box element written q-th
-//   LEGO_FN IDX_T bsrc(IDX_T i, IDX_T j), bdst(IDX_T i, IDX_T j)   element
-//                                    offsets of logical point (i, j)
+//   S_SEP, LEGO_FN IDX_T s_u(IDX_T bi, IDX_T bj, IDX_T r), s_l(IDX_T l)   1: the
+//                    source offset of lane l on row, column or antidiagonal r
+//                    of box (bi, bj) is s_u(bi, bj, r) + s_l(l); 0: LEGO_FN
+//                    IDX_T s_f(IDX_T i, IDX_T j) of logical point (i, j)
+//   D_SEP, d_u, d_l, d_f  the same for the destination
 // NONTEMPORAL: bit 0 streams (non-temporal) global loads, bit 1 stores.
 
 #if NONTEMPORAL & 1
@@ -134,39 +138,142 @@ extern "C" __global__ __launch_bounds__(NT) void lego_remap_lds(const ELEM_T* __
 #endif
 
 #ifdef LEGO_REMAP_BOX
-// One workgroup per box.  The read order makes consecutive lanes read
-// consecutive source addresses, the write order consecutive destination
-// addresses (runs of up to a box side); each LDS row is BC + BPAD elements,
-// the pad chosen so that neither order puts two lanes of a wave on one bank.
-// Points past the logical extents (boxes on the last row or column) are
-// neither read nor written.
-#define BOX (BR * BC)
-extern "C" __global__ __launch_bounds__(NT) void lego_remap_box(const ELEM_T* __restrict__ src,
-                                                                ELEM_T* __restrict__ dst) {
-  __shared__ ELEM_T tile[BR * (BC + BPAD)];
-  IDX_T bi, bj;
-  bord((IDX_T)blockIdx.x, &bi, &bj);
-  const IDX_T i0 = bi * BR, j0 = bj * BC;
-  const bool whole = i0 + BR <= EXT0 && j0 + BC <= EXT1;
-  ELEM_T v[BOX / NT];
-  IDX_T slot[BOX / NT];
-  // All reads first, so that BOX / NT loads per thread are in flight at once.
-#pragma unroll
-  for (int u = 0; u < BOX / NT; ++u) {
-    IDX_T a, b;
-    ws((IDX_T)(u * NT + threadIdx.x), &a, &b);
-    slot[u] = a * (BC + BPAD) + b;
-    if (whole || (i0 + a < EXT0 && j0 + b < EXT1)) v[u] = LEGO_LD(src + bsrc(i0 + a, j0 + b));
+// One workgroup (NT threads, NT/64 waves) per BX x BX box of the logical
+// index space (BX = 64 or 128), staged through LDS.  Each side is copied line
+// by line; lane l of a wave takes positions x = l, l + 64, ... (EPL of them)
+// of line p of the box, a line being
+//   ORD 0: box row p:    (a, b) = (p, x),
+//   ORD 1: box column p: (a, b) = (x, p),
+//   ORD 2: box antidiagonals p and p + BX together (their lengths add up to
+//          BX): (a, b) = (x, (p - x) mod BX), on antidiagonal p for x <= p
+//          and on antidiagonal p + BX for x > p, so every position is used.
+// Wave w copies lines w, w + NT/64, ...  Where the planner split a side's
+// element offset into a part of (box, row or column or antidiagonal r) and a
+// part of the position x (S_SEP, D_SEP), an element costs one add: the parts
+// of every r are computed once per box, r = 64k + q in lane q of table k, and
+// read out of that lane for each line; otherwise the offset is s_f(i, j) of
+// the point.  Points past the logical extents (boxes on the last row or
+// column) are neither read nor written.  Each LDS row is BX + BPAD elements,
+// the pad chosen against bank conflicts of both kinds of line.
+#define NW (NT / 64)
+#define EPL (BX / 64)
+#define NITER (BX / NW)
+#define NTAB(o) ((o) == 2 ? 2 * EPL : EPL)
+template <bool B>
+struct lego_flag {
+  static constexpr bool value = B;
+};
+// Lane q's value of x (x holds one value per lane).
+LEGO_FN IDX_T lane_read(IDX_T x, IDX_T q) {
+  if (sizeof(IDX_T) == 8) {
+    const u64 v = (u64)x;
+    const u32 lo = (u32)__builtin_amdgcn_readlane((int)(u32)v, (int)q);
+    const u32 hi = (u32)__builtin_amdgcn_readlane((int)(u32)(v >> 32), (int)q);
+    return (IDX_T)(((u64)hi << 32) | lo);
   }
-#pragma unroll
-  for (int u = 0; u < BOX / NT; ++u) tile[slot[u]] = v[u];
-  __syncthreads();
-#pragma unroll
-  for (int u = 0; u < BOX / NT; ++u) {
-    IDX_T a, b;
-    wd((IDX_T)(u * NT + threadIdx.x), &a, &b);
-    if (whole || (i0 + a < EXT0 && j0 + b < EXT1)) LEGO_ST(tile[a * (BC + BPAD) + b], dst + bdst(i0 + a, j0 + b));
+  return (IDX_T)(u32)__builtin_amdgcn_readlane((int)x, (int)q);
+}
+template <int ORD>
+LEGO_FN void box_pt(IDX_T p, IDX_T x, IDX_T* a, IDX_T* b) {
+  if (ORD == 0) {
+    *a = p;
+    *b = x;
+  } else if (ORD == 1) {
+    *a = x;
+    *b = p;
+  } else {
+    *a = x;
+    *b = (p - x) & (BX - 1);
   }
 }
-#undef BOX
+// Offset of position x = l + 64 e of line p (it-th line of this wave) of a
+// side whose offset is split: the part of its row, column or antidiagonal,
+// read out of its lane of the tables, plus the position's part.
+template <int ORD>
+LEGO_FN IDX_T line_off(const IDX_T* tab, const IDX_T* xpart, int it, int e, IDX_T p, IDX_T x) {
+  const int k = it * NW / 64;  // p / 64: every line of one iteration is in one table
+  const IDX_T q = p % 64u;
+  if (ORD == 2) {
+    const IDX_T lo = lane_read(tab[k], q), hi = lane_read(tab[k + EPL], q);
+    return (x <= p ? lo : hi) + xpart[e];
+  }
+  return lane_read(tab[k], q) + xpart[e];
+}
+extern "C" __global__ __launch_bounds__(NT) void lego_remap_box(const ELEM_T* __restrict__ src,
+                                                                ELEM_T* __restrict__ dst) {
+  __shared__ ELEM_T tile[BX * (BX + BPAD)];
+  IDX_T bi, bj;
+  bord((IDX_T)blockIdx.x, &bi, &bj);
+  const IDX_T i0 = bi * BX, j0 = bj * BX;
+  const bool whole = i0 + BX <= EXT0 && j0 + BX <= EXT1;
+  const IDX_T l = threadIdx.x % 64u;
+  const IDX_T w = __builtin_amdgcn_readfirstlane(threadIdx.x / 64u);
+#if S_SEP
+  IDX_T s_tab[NTAB(S_ORD)], s_x[EPL];
+#pragma unroll
+  for (int k = 0; k < NTAB(S_ORD); ++k) s_tab[k] = s_u(bi, bj, 64u * k + l);
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) s_x[e] = s_l(l + 64u * e);
+#endif
+#if D_SEP
+  IDX_T d_tab[NTAB(D_ORD)], d_x[EPL];
+#pragma unroll
+  for (int k = 0; k < NTAB(D_ORD); ++k) d_tab[k] = d_u(bi, bj, 64u * k + l);
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) d_x[e] = d_l(l + 64u * e);
+#endif
+  // All loads first, NITER * EPL in flight per thread; boxes inside the
+  // extents (all but the last row and column of boxes) without any test.
+  ELEM_T v[NITER][EPL];
+  auto load = [&](auto checked) {
+#pragma unroll
+    for (int it = 0; it < NITER; ++it)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const IDX_T p = (IDX_T)it * NW + w, x = l + 64u * e;
+        IDX_T a, b;
+        box_pt<S_ORD>(p, x, &a, &b);
+        if (decltype(checked)::value && !(i0 + a < EXT0 && j0 + b < EXT1)) continue;
+#if S_SEP
+        v[it][e] = LEGO_LD(src + line_off<S_ORD>(s_tab, s_x, it, e, p, x));
+#else
+        v[it][e] = LEGO_LD(src + s_f(i0 + a, j0 + b));
+#endif
+      }
+  };
+  if (whole) load(lego_flag<false>{});
+  else load(lego_flag<true>{});
+#pragma unroll
+  for (int it = 0; it < NITER; ++it)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const IDX_T p = (IDX_T)it * NW + w, x = l + 64u * e;
+      IDX_T a, b;
+      box_pt<S_ORD>(p, x, &a, &b);
+      tile[a * (BX + BPAD) + b] = v[it][e];
+    }
+  __syncthreads();
+  auto store = [&](auto checked) {
+#pragma unroll
+    for (int it = 0; it < NITER; ++it)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const IDX_T p = (IDX_T)it * NW + w, x = l + 64u * e;
+        IDX_T a, b;
+        box_pt<D_ORD>(p, x, &a, &b);
+        if (decltype(checked)::value && !(i0 + a < EXT0 && j0 + b < EXT1)) continue;
+#if D_SEP
+        LEGO_ST(tile[a * (BX + BPAD) + b], dst + line_off<D_ORD>(d_tab, d_x, it, e, p, x));
+#else
+        LEGO_ST(tile[a * (BX + BPAD) + b], dst + d_f(i0 + a, j0 + b));
+#endif
+      }
+  };
+  if (whole) store(lego_flag<false>{});
+  else store(lego_flag<true>{});
+}
+#undef NTAB
+#undef NITER
+#undef EPL
+#undef NW
 #endif

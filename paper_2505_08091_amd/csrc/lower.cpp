@@ -11,7 +11,7 @@ std::string fn_text(const Ctx& c, const std::string& name, const FnSpec& f, bool
   bool w = force_wide;
   for (size_t k = 0; k < f.outs.size(); ++k) {
     const bool bounded = k < f.out_bound.size() && f.out_bound[k] > 0 && f.out_bound[k] <= (i64(1) << 32);
-    w = w || !(bounded ? ring32(f.outs[k]) : fits32(f.outs[k]));
+    w = w || !(bounded || f.ring_out ? ring32(f.outs[k]) : fits32(f.outs[k]));
   }
   for (int v : f.params) w = w || c.vars[v].hi >= (i64(1) << 32);
   const char* T = w ? "i64" : "u32";

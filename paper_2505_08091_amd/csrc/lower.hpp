@@ -25,6 +25,10 @@ struct FnSpec {
   // inverse within its extents, its forward map within its physical size),
   // which lets 32-bit code compute it through out-of-range intermediates.
   std::vector<i64> out_bound;
+  // The caller uses the outputs only modulo 2^32: they are parts of a sum
+  // whose total lies in [0, 2^32), so 32-bit code may compute each part
+  // through out-of-range values as long as it is right modulo 2^32.
+  bool ring_out = false;
 };
 
 struct Emitted {

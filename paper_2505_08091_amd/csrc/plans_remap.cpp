@@ -184,57 +184,79 @@ RemapPlan plan_remap(const Layout& src, const Layout& dst, int elem_bytes) {
 }
 
 // Box-staged remap for 2-D maps without digit structure (an element gather
-// otherwise; e.g. Row <-> antidiagonal order).  A B x B box of the logical
-// index space goes through LDS: its elements are read in the order ws (a
-// layout over the box) under which the source layout is most contiguous, and
-// written in the order wd under which the destination layout is.  The orders
-// are chosen among Row, Col and the antidiagonal GenP of the box by counting,
-// on the host, the breaks in the address sequence over a sample box.  Returns
-// false when no order gives runs of 8 elements on average on both sides.
+// otherwise; e.g. Row <-> antidiagonal order).  A 64 x 64 box of the logical
+// index space goes through LDS.  Each side is copied line by line, a line
+// being a row, a column or an antidiagonal of the box with a wave's lanes
+// along it; for each side the planner picks the kind of line under which that
+// side's layout is most contiguous (counting, on the host, the breaks in the
+// address sequence of a sample box).  It then tries to split the side's
+// element offset L(64 bi + a, 64 bj + b) into a part of (box, line) and a part
+// of the lane, so that an element costs one add: along an antidiagonal a + b
+// is the line's, and the antidiagonal order of Figure 7 is then the line's
+// start plus the row.  Returns false when no kind of line gives runs of 8
+// elements on average on both sides.
 static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes, RemapPlan* out) {
   const std::vector<i64> n = src.dims();
   if (n.size() != 2) return false;
-  const i64 B = elem_bytes <= 4 ? 64 : 32;
-  if (n[0] < B || n[1] < B) return false;
-  const std::vector<std::pair<std::string, LayoutP>> orders = {
-      {"row", make_from_piece(make_row({B, B}))},
-      {"col", make_from_piece(make_col({B, B}))},
-      {"antidiag", make_from_piece(make_genp(GEN_ANTIDIAG, {B, B}, {}))}};
+  if (n[0] < 64 || n[1] < 64) return false;
+  // Remaps whose traffic exceeds the 256 MB last-level cache go to HBM: there
+  // 128 x 128 boxes (longer runs per row visited, fewer partly written cache
+  // lines along antidiagonals); smaller remaps keep 64 x 64 boxes (more of
+  // them in flight: 4096^2 fp32 antidiagonal -> Row 5.3 -> 6.1 TB/s), as do
+  // 8-byte elements (LDS and registers).
+  const bool beyond_llc = 2 * n[0] * n[1] * elem_bytes > (i64(256) << 20);
+  const i64 B = tune("remap.box_side", beyond_llc && n[0] >= 128 && n[1] >= 128 && elem_bytes <= 4 ? 128 : 64);
+  const char* names[3] = {"rows", "cols", "antidiags"};
+  // Box element (a, b) of lane l on line p: row p, column p, or the pair of
+  // antidiagonals p and p + 64 (a + b = p for l <= p, p + 64 after), whose
+  // lengths add up to 64.  r: the row, column or antidiagonal it lies on.
+  auto pt = [&](int ord, i64 p, i64 l, i64* a, i64* b) {
+    if (ord == 0) *a = p, *b = l;
+    else if (ord == 1) *a = l, *b = p;
+    else *a = l, *b = (p - l) & (B - 1);
+  };
+  const i64 nparts[3] = {B, B, 2 * B - 1};  // rows, columns, antidiagonals
   // A box away from the edges when there is one (the first otherwise).
   const i64 o0 = n[0] >= 3 * B ? B : 0, o1 = n[1] >= 3 * B ? B : 0;
-  auto breaks = [&](const Layout& L, const Layout& W) {
-    i64 prev = 0, nb = 0;
-    for (i64 q = 0; q < B * B; ++q) {
-      const std::vector<i64> ab = host_inv(W, q);
-      const i64 x = host_apply(L, {o0 + ab[0], o1 + ab[1]});
-      if (q == 0 || x != prev + 1) ++nb;
-      prev = x;
+  auto breaks = [&](const Layout& L, int ord) {
+    i64 nb = 0;
+    for (i64 p = 0; p < B; ++p) {
+      i64 prev = 0;
+      for (i64 l = 0; l < B; ++l) {
+        i64 a, b;
+        pt(ord, p, l, &a, &b);
+        const i64 x = host_apply(L, {o0 + a, o1 + b});
+        if (l == 0 || x != prev + 1) ++nb;
+        prev = x;
+      }
     }
     return nb;
   };
-  size_t ws = 0, wd = 0;
+  int os = 0, od = 0;
   i64 bs = -1, bd = -1;
-  for (size_t k = 0; k < orders.size(); ++k) {
-    const i64 x = breaks(src, *orders[k].second), y = breaks(dst, *orders[k].second);
-    if (bs < 0 || x < bs) bs = x, ws = k;
-    if (bd < 0 || y < bd) bd = y, wd = k;
+  for (int k = 0; k < 3; ++k) {
+    const i64 x = breaks(src, k), y = breaks(dst, k);
+    if (bs < 0 || x < bs) bs = x, os = k;
+    if (bd < 0 || y < bd) bd = y, od = k;
   }
   if (bs * 8 > B * B || bd * 8 > B * B) return false;
   // LDS slot of box element (a, b): a * (B + pad) + b, with the pad that
-  // keeps the 64 lanes of a wave on distinct 4-byte banks under both orders
-  // (Row/antidiagonal: 0, strides 1 and B-1; Col needs a pad).
+  // keeps the lanes of a wave on distinct 4-byte banks under both kinds of
+  // line where it can (rows: stride 1; columns: B + pad; antidiagonals:
+  // B + pad - 1).
   int pad = 0;
   {
     int best = 1 << 30;
     for (int pd = 0; pd < 4; ++pd) {
       int cost = 0;
-      for (size_t k : {ws, wd})
-        for (i64 q0 : {i64(0), B * B / 2}) {
+      for (int k : {os, od})
+        for (i64 p : {i64(0), B / 2}) {
           std::vector<int> hits(64, 0);
           int worst = 0;
           for (i64 l = 0; l < 64; ++l) {
-            const std::vector<i64> ab = host_inv(*orders[k].second, q0 + l);
-            const i64 slot = ab[0] * (B + pd) + ab[1];
+            i64 a, b;
+            pt(k, p, l, &a, &b);
+            const i64 slot = a * (B + pd) + b;
             worst = std::max(worst, ++hits[(slot * elem_bytes / 4) % 64]);
           }
           cost += worst;
@@ -244,14 +266,13 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
   }
   const int NT = 256;
   const i64 nbr = (n[0] + B - 1) / B, nbc = (n[1] + B - 1) / B, nb = nbr * nbc;
-  const LayoutP Ws = orders[ws].second, Wd = orders[wd].second;
   // Box order, a layout over the grid of boxes.  A run along an antidiagonal
   // ends mid-line at a box edge and the rest of the line belongs to the next
-  // box along the antidiagonal, so with an antidiagonal order inside boxes the
-  // boxes go in antidiagonal order too; workgroups are dispatched round-robin
-  // over the 8 XCDs, so XCD x takes the x-th eighth of that order and the
-  // boxes that share lines share its L2.
-  const bool ad_boxes = (orders[ws].first == "antidiag" || orders[wd].first == "antidiag") && nbr == nbc;
+  // box along the antidiagonal, so with antidiagonal lines the boxes go in
+  // antidiagonal order too; workgroups are dispatched round-robin over the 8
+  // XCDs, so XCD x takes the x-th eighth of that order and the boxes that
+  // share lines share its L2.
+  const bool ad_boxes = (os == 2 || od == 2) && nbr == nbc;
   const bool xcd = nb % 8 == 0;
   const LayoutP Wb = ad_boxes ? make_from_piece(make_genp(GEN_ANTIDIAG, {nbr, nbc}, {})) : make_from_piece(make_row({nbr, nbc}));
   auto box_fn = [&](Ctx& c) {
@@ -265,14 +286,48 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
     f.out_bound = {nbr, nbc};
     return f;
   };
-  auto order_fn = [&](const LayoutP& W) {
-    return [&, W](Ctx& c) {
-      int q = c.var("q", B * B);
-      SymAlg al{&c};
+  // Element offset of lane l on row, column or antidiagonal r of box (bi,
+  // bj) as a Sum (on antidiagonal r the lane's element is (l, r - l)), and its
+  // split into a (box, r) part and a lane part.
+  auto side = [&](Ctx& c, const Layout& L, int ord, int* bi, int* bj, int* r, int* l) {
+    *bi = c.var("bi", nbr);
+    *bj = c.var("bj", nbc);
+    *r = c.var("r", nparts[ord]);
+    *l = c.var("l", B);
+    Sum a, b;
+    if (ord == 0) a = var(c, *r), b = var(c, *l);
+    else if (ord == 1) a = var(c, *l), b = var(c, *r);
+    else a = var(c, *l), b = sub(c, var(c, *r), var(c, *l));
+    SymAlg al{&c};
+    return L.apply(al, {add(c, mulc(c, var(c, *bi), B), a), add(c, mulc(c, var(c, *bj), B), b)});
+  };
+  auto separable = [&](const Layout& L, int ord) {
+    try {
+      Ctx c;
+      int bi, bj, r, l;
+      Sum off = side(c, L, ord, &bi, &bj, &r, &l), lane, rest;
+      return split_by(off, {l}, &lane, &rest);
+    } catch (const std::exception&) {
+      return false;
+    }
+  };
+  const bool ssep = separable(src, os), dsep = separable(dst, od);
+  auto part_fn = [&](const Layout* L, int ord, bool lane_part) {
+    return [&, L, ord, lane_part](Ctx& c) {
+      int bi, bj, r, l;
+      Sum off = side(c, *L, ord, &bi, &bj, &r, &l), lane, rest;
       FnSpec f;
-      f.params = {q};
-      f.outs = W->inv(al, var(c, q));
-      f.out_bound = {B, B};
+      f.valid = split_by(off, {l}, &lane, &rest);
+      // the kernel adds the two parts in the index type, and their total is
+      // an offset of the side's buffer
+      f.ring_out = L->phys_size() <= (i64(1) << 32);
+      if (lane_part) {
+        f.params = {l};
+        f.outs = {lane};
+      } else {
+        f.params = {bi, bj, r};
+        f.outs = {rest};
+      }
       return f;
     };
   };
@@ -287,19 +342,40 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
       return f;
     };
   };
+  std::vector<std::pair<std::string, std::function<FnSpec(Ctx&)>>> fns = {{"bord", box_fn}};
+  std::vector<std::string> parts;
+  if (ssep) {
+    fns.push_back({"s_u", part_fn(&src, os, false)});
+    fns.push_back({"s_l", part_fn(&src, os, true)});
+    parts.insert(parts.end(), {"s_u", "s_l"});
+  } else {
+    fns.push_back({"s_f", addr_fn(&src)});
+  }
+  if (dsep) {
+    fns.push_back({"d_u", part_fn(&dst, od, false)});
+    fns.push_back({"d_l", part_fn(&dst, od, true)});
+    parts.insert(parts.end(), {"d_u", "d_l"});
+  } else {
+    fns.push_back({"d_f", addr_fn(&dst)});
+  }
   std::string info;
   bool wide = false;
-  std::string fns = emit_all({{"bord", box_fn}, {"ws", order_fn(Ws)}, {"wd", order_fn(Wd)}, {"bsrc", addr_fn(&src)},
-                              {"bdst", addr_fn(&dst)}},
-                             &wide, &info);
+  std::string code = emit_all(fns, &wide, &info, parts);
+  // Beyond the last-level cache, the side copied along rows or columns
+  // streams (non-temporal), which leaves the cache to the other side's
+  // antidiagonal segments, whose partly covered lines the neighbouring boxes
+  // complete (8192^2 fp32 with 128 x 128 boxes: Row <-> antidiagonal 3.9 /
+  // 4.1 -> 5.3 / 5.9 TB/s; within the cache it costs 10-15%).
   int nontemporal = 0;
+  if (beyond_llc && (os == 2) != (od == 2)) nontemporal = os == 2 ? 2 : 1;
   nontemporal = (int)tune("remap.nontemporal", nontemporal);
   std::ostringstream s;
   s << header() << "#define ELEM_T " << elem_type(elem_bytes) << "\n#define IDX_T " << (wide ? "i64" : "u32")
-    << "\n#define BR " << B << "\n#define BC " << B << "\n#define BPAD " << pad << "\n#define NBR " << nbr << "\n#define NBC " << nbc
-    << "\n#define EXT0 " << n[0] << "\n#define EXT1 " << n[1] << "\n#define NT " << NT
-    << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_BOX 1\n"
-    << fns << "// ---- template ----\n" << tpl_remap;
+    << "\n#define BX " << B << "\n#define BPAD " << pad << "\n#define NBR " << nbr << "\n#define NBC " << nbc << "\n#define EXT0 " << n[0]
+    << "\n#define EXT1 " << n[1] << "\n#define NT " << NT << "\n#define S_ORD " << os << "\n#define D_ORD " << od
+    << "\n#define S_SEP " << (ssep ? 1 : 0) << "\n#define D_SEP " << (dsep ? 1 : 0) << "\n#define NONTEMPORAL "
+    << nontemporal << "\n#define LEGO_REMAP_BOX 1\n"
+    << code << "// ---- template ----\n" << tpl_remap;
   RemapPlan& R = *out;
   R.path = REMAP_BOX;
   R.run = 1;
@@ -307,12 +383,13 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
   R.tile = B * B;
   R.kernel = "lego_remap_box";
   R.block = NT;
-  R.grid = nbr * nbc;
+  R.grid = nb;
   R.src = s.str();
   R.info = "box " + std::to_string(B) + "x" + std::to_string(B) + (ad_boxes ? " antidiag" : " row") +
-           (xcd ? "-xcd" : "") + " order load " + orders[ws].first + " (" +
-           std::to_string(bs) + " runs) store " + orders[wd].first + " (" + std::to_string(bd) + " runs) pad " +
-           std::to_string(pad) + " NT=" + std::to_string(NT) + info;
+           (xcd ? "-xcd" : "") + " load " + names[os] + (ssep ? " sep" : " full") + " (" + std::to_string(bs) +
+           " runs) store " + names[od] + (dsep ? " sep" : " full") + " (" + std::to_string(bd) + " runs) pad " +
+           std::to_string(pad) + (nontemporal & 1 ? " nt-loads" : "") + (nontemporal & 2 ? " nt-stores" : "") +
+           " NT=" + std::to_string(NT) + info;
   return true;
 }
 

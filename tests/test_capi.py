@@ -170,9 +170,15 @@ def test_plans_choose_expected_paths(lego):
     n = 4096
     row, ad = L.as_layout(L.Row(n, n)), L.as_layout(L.GenP("antidiag", [n, n]))
     p = L.remap_plan(row, ad, 4)
-    assert p["path"] == "box" and p["tile"] == 4096 and "load row (64 runs) store antidiag (127 runs)" in p["info"]
+    assert p["path"] == "box" and p["tile"] == 4096 and "load rows sep (64 runs) store antidiags sep (127 runs)" in p["info"]
     p = L.remap_plan(ad, row, 4)
-    assert p["path"] == "box" and "load antidiag (127 runs) store row (64 runs)" in p["info"]
+    assert p["path"] == "box" and "load antidiags sep (127 runs) store rows sep (64 runs)" in p["info"]
+    # beyond the last-level cache: 128 x 128 boxes, the row side streaming
+    n = 8192
+    row, ad = L.as_layout(L.Row(n, n)), L.as_layout(L.GenP("antidiag", [n, n]))
+    p = L.remap_plan(row, ad, 4)
+    assert p["tile"] == 128 * 128 and "nt-loads" in p["info"] and "store antidiags sep" in p["info"]
+    assert "nt-stores" in L.remap_plan(ad, row, 4)["info"]
     info = L.gemm_plan(8192, 8192, 8192, "bf16")
     assert "direct-lds spread fd2" in info and "A:V8k sep" in info and "frvec" in info
     assert "waves 2x2 wave 128x128" in info

@@ -71,44 +71,66 @@ int main(int argc, char** argv) {
     for (int e = 0; e < V; ++e) perm[t * V + e] = (long long)(s * V + e);
   }
 #elif defined(LEGO_REMAP_BOX)
+  // The box kernel's lines (emulated): position l of line p of a BX x BX box;
+  // the per-side offsets from the generated functions, split or whole.
   const u64 n = (u64)EXT0 * EXT1, nsrc = n;
-  if ((BR * BC) % NT || NT > 256) FAIL("NT does not divide the box");
-  if ((unsigned long long)BR * (BC + BPAD) * sizeof(ELEM_T) > 65536) FAIL("box exceeds 64 KiB of LDS");
-  if (NBR != (EXT0 + BR - 1) / BR || NBC != (EXT1 + BC - 1) / BC) FAIL("box grid does not cover the extents");
+  const long long NW = NT / 64;
+  if (NT % 64 || NT > 256) FAIL("NT is not whole waves");
+  if ((unsigned long long)BX * (BX + BPAD) * sizeof(ELEM_T) > 160 * 1024) FAIL("box exceeds 160 KiB of LDS");
+  if (NBR != (EXT0 + BX - 1) / BX || NBC != (EXT1 + BX - 1) / BX) FAIL("box grid does not cover the extents");
+  // position l on line p: row p, column p, or antidiagonals p (l <= p) and
+  // p + BX (l > p); r is the row, column or antidiagonal of the element
+  auto pt = [&](int ord, long long p, long long l, long long* a, long long* b, long long* r) {
+    if (ord == 0) { *a = p; *b = l; *r = p; }
+    else if (ord == 1) { *a = l; *b = p; *r = p; }
+    else { *a = l; *b = (p - l) & (BX - 1); *r = *a + *b; }
+  };
   std::vector<long long> perm(n, -2);
-  std::vector<long long> tile((u64)BR * (BC + BPAD));
+  std::vector<long long> tile((u64)BX * (BX + BPAD));
   std::vector<char> bseen((u64)NBR * NBC);
   for (u64 bx = 0; bx < (u64)NBR * NBC; ++bx) {
     IDX_T bi, bj;
     bord((IDX_T)bx, &bi, &bj);
     if (bi >= NBR || bj >= NBC || bseen[(u64)bi * NBC + bj]++) FAIL("bord is not a bijection onto the boxes");
-    const u64 i0 = (u64)bi * BR, j0 = (u64)bj * BC;
+    const u64 i0 = (u64)bi * BX, j0 = (u64)bj * BX;
     std::fill(tile.begin(), tile.end(), -1);
-    std::vector<char> rseen(BR * BC), wseen(BR * BC);
-    for (u64 q = 0; q < (u64)BR * BC; ++q) {
-      IDX_T a, b;
-      ws((IDX_T)q, &a, &b);
-      if (a >= BR || b >= BC) FAIL("ws(%llu) outside the box", (unsigned long long)q);
-      if (rseen[a * BC + b]++) FAIL("ws is not a bijection onto the box");
-      if (i0 + a < EXT0 && j0 + b < EXT1) {
-        u64 s = (u64)bsrc((IDX_T)(i0 + a), (IDX_T)(j0 + b));
-        if (s >= nsrc) FAIL("bsrc out of range");
-        tile[a * (BC + BPAD) + b] = (long long)s;
-      }
-    }
-    for (u64 q = 0; q < (u64)BR * BC; ++q) {
-      IDX_T a, b;
-      wd((IDX_T)q, &a, &b);
-      if (a >= BR || b >= BC) FAIL("wd(%llu) outside the box", (unsigned long long)q);
-      if (wseen[a * BC + b]++) FAIL("wd is not a bijection onto the box");
-      if (i0 + a < EXT0 && j0 + b < EXT1) {
-        u64 d = (u64)bdst((IDX_T)(i0 + a), (IDX_T)(j0 + b));
-        if (d >= n) FAIL("bdst out of range");
-        if (perm[d] != -2) FAIL("destination written twice");
-        if (tile[a * (BC + BPAD) + b] < 0) FAIL("LDS slot read before written");
-        perm[d] = tile[a * (BC + BPAD) + b];
-      }
-    }
+    std::vector<char> rseen(BX * BX), wseen(BX * BX);
+    for (long long it = 0; it * NW < BX; ++it)
+      for (long long w = 0; w < NW; ++w)
+        for (long long l = 0; l < BX; ++l) {  // position l of the line (lane l % 64)
+          const long long p = it * NW + w;
+          long long a, b, r;
+          pt(S_ORD, p, l, &a, &b, &r);
+          if (rseen[a * BX + b]++) FAIL("a box point is loaded twice");
+          if (i0 + a >= (u64)EXT0 || j0 + b >= (u64)EXT1) continue;
+#if S_SEP
+          const u64 sa = (u64)(IDX_T)(s_u(bi, bj, (IDX_T)r) + s_l((IDX_T)l));
+#else
+          const u64 sa = (u64)s_f((IDX_T)(i0 + a), (IDX_T)(j0 + b));
+#endif
+          if (sa >= nsrc) FAIL("source offset out of range");
+          tile[a * (BX + BPAD) + b] = (long long)sa;
+        }
+    for (long long it = 0; it * NW < BX; ++it)
+      for (long long w = 0; w < NW; ++w)
+        for (long long l = 0; l < BX; ++l) {  // position l of the line (lane l % 64)
+          const long long p = it * NW + w;
+          long long a, b, r;
+          pt(D_ORD, p, l, &a, &b, &r);
+          if (wseen[a * BX + b]++) FAIL("a box point is stored twice");
+          if (i0 + a >= (u64)EXT0 || j0 + b >= (u64)EXT1) continue;
+#if D_SEP
+          const u64 d = (u64)(IDX_T)(d_u(bi, bj, (IDX_T)r) + d_l((IDX_T)l));
+#else
+          const u64 d = (u64)d_f((IDX_T)(i0 + a), (IDX_T)(j0 + b));
+#endif
+          if (d >= n) FAIL("destination offset out of range");
+          if (perm[d] != -2) FAIL("destination written twice");
+          if (tile[a * (BX + BPAD) + b] < 0) FAIL("LDS slot read before written");
+          perm[d] = tile[a * (BX + BPAD) + b];
+        }
+    for (long long q = 0; q < BX * BX; ++q)
+      if (!rseen[q] || !wseen[q]) FAIL("a box point is not covered by the lines");
   }
 #else
   const u64 n = NELEM, nsrc = NELEM;
@@ -365,6 +387,8 @@ def _oracle_for(name):
         "remap row->morton f16": ("remap", r4, mz),
         "remap morton->row f16": ("remap", mz, r4),
         "remap row->col f32": ("remap", row8, OL.as_layout(OL.Col(8192, 8192))),
+        "remap row->antidiag f32": ("remap", OL.as_layout(OL.Row(4096, 4096)), OL.as_layout(OL.antidiag_genp(4096))),
+        "remap antidiag->row f32": ("remap", OL.as_layout(OL.antidiag_genp(4096)), OL.as_layout(OL.Row(4096, 4096))),
     }.get(name)
 
 
@@ -381,7 +405,7 @@ def _compile_and_run(src, harness, tmp, args=()):
     return r.stdout
 
 
-N_SOURCES = 13
+N_SOURCES = 15
 
 
 def test_source_count():
