@@ -498,6 +498,82 @@ def bench_extra(L, reps=20):
     return out
 
 
+def _remap_pair(L, name):
+    """The two layouts, element size and size of a named remap workload."""
+    kind, dt, n = name.split("_")[0], name.split("_")[1], int(name.split("_")[2])
+    row = L.as_layout(L.Row(n, n))
+    other = {"transpose": lambda: L.as_layout(L.Col(n, n)),
+             "morton": lambda: L.as_layout(L.GenP("morton", [n, n])),
+             "antidiag": lambda: L.as_layout(L.GenP("antidiag", [n, n])),
+             "blocked": lambda: L.TileOrderBy(L.Col(n // 64, n // 64), L.Row(64, 64)),
+             "identity": lambda: row}[kind]()
+    return row, other, dt, n
+
+
+WORKLOADS = ("remap: blocked_f32_8192, transpose_f32_{2048,4096,8192}, morton_f16_4096, antidiag_f32_{4096,8192}, "
+             "identity_f32_8192 (a plain copy) "
+             "(suffix _fwd or _inv: one direction only, its source fixed; _flushed: a 1 GiB fill evicts the "
+             "last-level cache before each launch); gemm: gemm_bf16_8192, gemm_morton_f16_4096")
+
+
+def run_workload(L, name, reps):
+    """``reps`` launches of one named workload and nothing else (for
+    rocprofv3 runs; see WORKLOADS).  Remaps alternate directions unless a
+    direction is named; returns the mean duration of each direction."""
+    import torch
+    import synth_inputs as S
+    if name == "gemm_bf16_8192":
+        g = bench_gemm(L, reps, 30)
+        return {"workload": name, "ms": round(g["ms"], 5), "tflops": round(g["tflops"], 1), "plan": g["plan"]}
+    if name.startswith("gemm_"):
+        dt, n = name.split("_")[2], int(name.split("_")[3])
+        a = S.tensor(n * n, dt, dist="normal", seed=S.SEED_A).cuda()
+        b = S.tensor(n * n, dt, dist="normal", seed=S.SEED_B).cuda()
+        c = torch.empty(n * n, dtype=torch.float32, device="cuda")
+        kw = {}
+        if "morton" in name:
+            mz = L.as_layout(L.GenP("morton", [n, n]))
+            a_mz = torch.empty_like(a)
+            L.remap(L.as_layout(L.Row(n, n)), mz, a, a_mz)
+            a, kw = a_mz, dict(a=mz, b=L.as_layout(L.Row(n, n)))
+        ms = _gemm_ms(L, a, b, c, n, dt, reps, warmup=10, **kw)
+        return {"workload": name, "ms": round(ms, 5), "tflops": round(2.0 * n ** 3 / ms / 1e9, 1),
+                "plan": L.gemm_plan(n, n, n, dt, **kw)}
+    base = name.replace("_fwd", "").replace("_inv", "").replace("_flushed", "")
+    row, other, dt, n = _remap_pair(L, base)
+    x = S.tensor(n * n, dt, seed=S.SEED_SRC).cuda()
+    y, z = torch.empty_like(x), torch.empty_like(x)
+    nb = 2 * n * n * x.element_size()
+    if name.endswith("_fwd") or name.endswith("_inv"):
+        la, lb = (row, other) if name.endswith("_fwd") else (other, row)
+        if name.endswith("_inv"):
+            L.remap(row, other, x, z)
+            x, z = z, x
+        for _ in range(5):
+            L.remap(la, lb, x, y)
+        ev = HipEvents(reps + 1, _stream())
+        torch.cuda.synchronize()
+        for k in range(reps):
+            ev.record(k)
+            L.remap(la, lb, x, y)
+        ev.record(reps)
+        torch.cuda.synchronize()
+        ms = ev.ms(0, reps) / reps
+        ev.close()
+        return {"workload": name, "ms": round(ms, 5), "GBps": round(nb / ms / 1e6, 1),
+                "plan": L.remap_plan(la, lb, x.element_size())["info"]}
+    if name.endswith("_flushed"):
+        L.remap(row, other, x, y)  # load both kernels before the timed launches
+        L.remap(other, row, y, z)
+        scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        f, i = _flushed(L, row, other, x, y, z, scratch, reps)
+    else:
+        f, i = _alternate(L, row, other, x, y, z, reps)
+    return {"workload": name, "fwd_ms": round(f, 5), "inv_ms": round(i, 5), "fwd_GBps": round(nb / f / 1e6, 1),
+            "inv_GBps": round(nb / i / 1e6, 1), "plan_fwd": L.remap_plan(row, other, x.element_size())["info"],
+            "plan_inv": L.remap_plan(other, row, x.element_size())["info"]}
+
+
 def cpu_baseline_remap(rounds=2):
     """The oracle remap of the full 8192^2 fp32 tensor, forward and back,
     ``rounds`` times, timed on this host."""
@@ -555,6 +631,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads (transposes, Morton, "
                                                             "operand-layout GEMMs)")
+    ap.add_argument("--workload", help="run only this workload, --steps launches (for profiling): " + WORKLOADS)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the layout remap and GEMM kernels run on a single MI355X; "
@@ -564,6 +641,9 @@ def main():
     import torch
     import paper_2505_08091_amd as L
     torch.cuda.set_device(0)
+    if args.workload:
+        print(json.dumps(run_workload(L, args.workload, args.steps)), flush=True)
+        return
 
     r = bench_remap(L, args.steps, args.warmup)
     ms_step = r["total_ms"] / args.steps

@@ -13,9 +13,15 @@
 //                                    ExpandBy source, Figure 9); else it is zero
 // LDS path (both sides are digit permutations; a tile of TILE elements is read
 // in source order into LDS and written in destination order):
-//   TILE, NT, VL, VS, LDSW_CONTIG
+//   TILE, NT, VL, VS, LDSW_CONTIG, LDS_BLOCK
 //   LEGO_FN IDX_T src_off(IDX_T g, IDX_T q)   element offset of source-side vector q of tile g
 //   LEGO_FN IDX_T ldsw(IDX_T q, IDX_T e)      LDS slot of element e of that vector
+//   LDS_BLOCK 1 (a transposing tile): a thread moves blocks of NX source
+//   vectors that hold NY whole destination vectors; then instead
+//   LEGO_FN IDX_T src_off(IDX_T g, IDX_T b, IDX_T x)  offset of load x of block b
+//   LEGO_FN IDX_T ldsw(IDX_T b, IDX_T y)      LDS slot of destination vector y of block b
+//   LEGO_FN int blk_el(int k)                 element k of destination vector k / VS
+//                                             is element blk_el(k) of the block's loads
 //   LEGO_FN IDX_T ldsr(IDX_T q)               LDS slot of destination-side vector q
 //   LEGO_FN IDX_T dst_off(IDX_T g, IDX_T q)   element offset of destination-side vector q
 // Box path (2-D maps without digit structure): a BX x BX box of the logical
@@ -109,6 +115,28 @@ extern "C" __global__ __launch_bounds__(NT) void lego_remap_lds(const ELEM_T* __
                                                                 ELEM_T* __restrict__ dst) {
   __shared__ ELEM_T tile[TILE];
   const IDX_T g = blockIdx.x;
+#if LDS_BLOCK
+  // Source-order phase by blocks: NX coalesced vector reads per block, a
+  // permutation in registers, NY whole destination vectors written to LDS.
+  vl_t v[TILE / (VL * NX) / NT][NX];
+#pragma unroll
+  for (int it = 0; it < TILE / (VL * NX) / NT; ++it) {
+    const IDX_T b = it * NT + threadIdx.x;
+#pragma unroll
+    for (int x = 0; x < NX; ++x) v[it][x] = LEGO_LD((const vl_t*)(src + src_off(g, b, (IDX_T)x)));
+  }
+#pragma unroll
+  for (int it = 0; it < TILE / (VL * NX) / NT; ++it) {
+    const IDX_T b = it * NT + threadIdx.x;
+#pragma unroll
+    for (int y = 0; y < NY; ++y) {
+      vs_t w;
+#pragma unroll
+      for (int e = 0; e < VS; ++e) w[e] = v[it][blk_el(y * VS + e) / VL][blk_el(y * VS + e) % VL];
+      *(vs_t*)&tile[ldsw(b, (IDX_T)y)] = w;
+    }
+  }
+#else
   // Source-order phase: coalesced vector reads, scattered LDS writes.
   vl_t v[TILE / VL / NT];
 #pragma unroll
@@ -126,6 +154,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_remap_lds(const ELEM_T* __
     for (int e = 0; e < VL; ++e) tile[ldsw(q, e)] = v[it][e];
 #endif
   }
+#endif
   __syncthreads();
   // Destination-order phase: vector LDS reads, coalesced vector writes.
 #pragma unroll

@@ -1,6 +1,9 @@
 // Planning of index-map evaluation and layout remap kernels.
 #include <algorithm>
+#include <functional>
+#include <map>
 #include <numeric>
+#include <set>
 #include <sstream>
 #include <stdexcept>
 
@@ -660,32 +663,28 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   // never emit a tile beyond 128 KiB of LDS (160 KiB per CU)
   if (TILE * elem_bytes > (128 << 10)) throw Unsupported("remap LDS tile exceeds 128 KiB");
   const i64 G = N / TILE;
-  // Tile-local orders.
+  // Tile-local orders and weights (recomputed after the digit splits below).
   std::vector<size_t> td, ts, gd;
-  for (size_t k = 0; k < d.size(); ++k) (d[k].tile ? td : gd).push_back(k);
-  // Tile order (the digit layout over tiles): source order for HBM-bound
-  // remaps, destination order otherwise.
+  std::vector<i64> wd, ws, wg;
   bool lds_src_order = hbm_bound;
   lds_src_order = tune("remap.order", lds_src_order) != 0;
-  if (lds_src_order) std::sort(gd.begin(), gd.end(), [&](size_t x, size_t y) { return d[x].c < d[y].c; });
-  ts = td;
-  std::sort(ts.begin(), ts.end(), [&](size_t x, size_t y) { return d[x].c < d[y].c; });
-  std::vector<i64> wd(d.size()), ws(d.size()), wg(d.size());
-  i64 w = 1;
-  for (size_t k : td) {
-    wd[k] = w;
-    w *= d[k].b;
-  }
-  w = 1;
-  for (size_t k : ts) {
-    ws[k] = w;
-    w *= d[k].b;
-  }
-  w = 1;
-  for (size_t k : gd) {
-    wg[k] = w;
-    w *= d[k].b;
-  }
+  auto orders = [&]() {
+    td.clear(), ts.clear(), gd.clear();
+    for (size_t k = 0; k < d.size(); ++k) (d[k].tile ? td : gd).push_back(k);
+    // Tile order (the digit layout over tiles): source order for HBM-bound
+    // remaps, destination order otherwise.
+    if (lds_src_order) std::sort(gd.begin(), gd.end(), [&](size_t x, size_t y) { return d[x].c < d[y].c; });
+    ts = td;
+    std::sort(ts.begin(), ts.end(), [&](size_t x, size_t y) { return d[x].c < d[y].c; });
+    wd.assign(d.size(), 0), ws.assign(d.size(), 0), wg.assign(d.size(), 0);
+    i64 w = 1;
+    for (size_t k : td) wd[k] = w, w *= d[k].b;
+    w = 1;
+    for (size_t k : ts) ws[k] = w, w *= d[k].b;
+    w = 1;
+    for (size_t k : gd) wg[k] = w, w *= d[k].b;
+  };
+  orders();
   // Vector widths: the leading tile digits that are contiguous on the source
   // (destination) side form runs; vectors must divide those runs.
   i64 srun = 1, drun = 1;
@@ -699,15 +698,95 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   }
   const int VL = pow2_vec(srun, maxv);
   const int VS = pow2_vec(drun, maxv);
-  // LDS tile rows of 256 bytes (all 64 banks once), in destination order.  The
+  // Split tile digits so that a source vector (the lowest VL of the tile's
+  // source order) and a destination vector (the lowest VS of its destination
+  // order) are made of whole digits.  Splitting a digit keeps the map; it
+  // only names the sub-ranges the block transfer below works with.
+  bool whole = true;
+  for (bool split = true; split && whole;) {
+    split = false;
+    for (int side = 0; side < 2 && !split && whole; ++side) {
+      i64 rem = side == 0 ? VL : VS;
+      for (size_t k : side == 0 ? ts : td) {
+        if (rem == 1) break;
+        if (rem % d[k].b == 0) {
+          rem /= d[k].b;
+          continue;
+        }
+        if (d[k].b % rem == 0) {
+          split_digit(d, k, rem);
+          orders();
+          split = true;
+        } else {
+          whole = false;
+        }
+        break;
+      }
+    }
+  }
+  // Digit classes: in the source vector (VL), in the destination vector (VS).
+  std::vector<char> in_vl(d.size()), in_vs(d.size());
+  if (whole) {
+    i64 r = 1;
+    for (size_t k : ts)
+      if (r < VL) in_vl[k] = 1, r *= d[k].b;
+    r = 1;
+    for (size_t k : td)
+      if (r < VS) in_vs[k] = 1, r *= d[k].b;
+  }
+  // Block transfer: a thread loads the NX source vectors that together hold
+  // NY whole destination vectors (the destination-vector digits outside the
+  // source vector, X, index the loads; the source-vector digits outside the
+  // destination vector, Y, index the stores), permutes them in registers,
+  // and writes whole destination vectors into LDS.  Both LDS phases are then
+  // vector accesses.  Taken when a destination vector spans several source
+  // vectors (a transposing tile) and a block fits a thread's share.
+  std::vector<size_t> xd, yd, bd;  // X (destination order), Y (source order), the rest (source order)
+  for (size_t k : td)
+    if (whole && in_vs[k] && !in_vl[k]) xd.push_back(k);
+  for (size_t k : ts) {
+    if (!whole) break;
+    if (in_vl[k] && !in_vs[k]) yd.push_back(k);
+    if (!in_vl[k] && !in_vs[k]) bd.push_back(k);
+  }
+  i64 NX = 1, NY = 1;
+  for (size_t k : xd) NX *= d[k].b;
+  for (size_t k : yd) NY *= d[k].b;
+  const i64 BLK = VL * NX;
+  // The loads stay coalesced only if the lanes of one load instruction, which
+  // walk the remaining digits in source order, cover whole 128-byte lines: a
+  // destination-vector digit low in the source order (Morton -> row) would
+  // leave gaps between the lanes' vectors.
+  i64 lane_run = VL;
+  for (size_t k : bd) {
+    if (d[k].c != lane_run) break;
+    lane_run *= d[k].b;
+  }
+  bool block = whole && NX >= 2 && VS >= 2 && BLK == VS * NY && BLK <= 64 && TILE % BLK == 0 &&
+               lane_run * elem_bytes >= 128;
+  block = block && tune("remap.block", 1) != 0;
+  std::vector<i64> wx(d.size()), wy(d.size()), wb(d.size());
+  {
+    i64 w = 1;
+    for (size_t k : xd) wx[k] = w, w *= d[k].b;
+    w = 1;
+    for (size_t k : yd) wy[k] = w, w *= d[k].b;
+    w = 1;
+    for (size_t k : bd) wb[k] = w, w *= d[k].b;
+  }
+  // LDS tile rows of 256 bytes, in destination order.  The
   // destination-side VS-vectors of a row are XOR-swizzled across rows (the
-  // swizzle is itself a GenP layout over [TILE/W, W]).  When the VL elements of
-  // a source vector land in VL consecutive rows (a transposing tile), the
-  // lanes of a wave differ in the row index above those VL rows, so the XOR
-  // takes row/VL: one lane group's scattered writes then cover distinct banks.
-  i64 W = std::max<i64>(VS, 256 / elem_bytes);
-  while (W > VS && TILE % W) W /= 2;
-  const bool swz = W / VS >= 2 && ((W / VS) & (W / VS - 1)) == 0 && TILE % W == 0;
+  // swizzle is itself a GenP layout over [TILE/W, W]): vector v of row r goes
+  // to position v ^ ((r / S) % (W / VS)).  S is chosen below by counting the
+  // bank conflicts of both LDS phases of one tile.
+  auto row_of = [&](i64 bytes) {
+    i64 w = std::max<i64>(VS, bytes / elem_bytes);
+    while (w > VS && TILE % w) w /= 2;
+    return w;
+  };
+  auto swizzles = [&](i64 w) { return w / VS >= 2 && ((w / VS) & (w / VS - 1)) == 0 && TILE % w == 0; };
+  i64 W = row_of(256);
+  bool swz = swizzles(W);
   auto digit_of = [&](Ctx& c, const Sum& x, i64 weight, i64 b) { return fmod(c, fdiv(c, x, weight), b); };
   auto kd_from_ks = [&](Ctx& c, const Sum& ks) {
     Sum kd = cst(0);
@@ -728,62 +807,10 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   }
   // A VL-run longer than a swizzled VS-vector may be split by the swizzle.
   if (VL > VS && swz) contig = false;
-  const i64 swz_s = contig ? 1 : VL;
-  PieceP sw = swz ? make_genp(GEN_XOR_SWIZZLE, {TILE / W, W}, {VS, swz_s}) : make_row({TILE / W, W});
-  LayoutP swl = make_from_piece(sw);
-  auto lds_slot = [&](Ctx& c, const Sum& kd) {
-    SymAlg al{&c};
-    return swl->apply(al, {fdiv(c, kd, W), fmod(c, kd, W)});
-  };
-  auto group_part = [&](Ctx& c, int g, bool dst_side) {
-    Sum o = cst(0);
-    for (size_t k : gd) o = add(c, o, mulc(c, digit_of(c, var(c, g), wg[k], d[k].b), dst_side ? d[k].a : d[k].c));
-    return o;
-  };
-  std::string fns = emit_all(
-      {{"src_off",
-        [&](Ctx& c) {
-          int g = c.var("g", G), q = c.var("q", TILE / VL);
-          Sum ks = mulc(c, var(c, q), VL);
-          Sum o = group_part(c, g, false);
-          for (size_t k : ts) o = add(c, o, mulc(c, digit_of(c, ks, ws[k], d[k].b), d[k].c));
-          FnSpec f;
-          f.params = {g, q};
-          f.outs = {o};
-          return f;
-        }},
-       {"ldsw",
-        [&](Ctx& c) {
-          int q = c.var("q", TILE / VL), e = c.var("e", VL);
-          Sum ks = add(c, mulc(c, var(c, q), VL), var(c, e));
-          FnSpec f;
-          f.params = {q, e};
-          f.outs = {lds_slot(c, kd_from_ks(c, ks))};
-          return f;
-        }},
-       {"ldsr",
-        [&](Ctx& c) {
-          int q = c.var("q", TILE / VS);
-          FnSpec f;
-          f.params = {q};
-          f.outs = {lds_slot(c, mulc(c, var(c, q), VS))};
-          return f;
-        }},
-       {"dst_off",
-        [&](Ctx& c) {
-          int g = c.var("g", G), q = c.var("q", TILE / VS);
-          Sum kd = mulc(c, var(c, q), VS);
-          Sum o = group_part(c, g, true);
-          for (size_t k : td) o = add(c, o, mulc(c, digit_of(c, kd, wd[k], d[k].b), d[k].a));
-          FnSpec f;
-          f.params = {g, q};
-          f.outs = {o};
-          return f;
-        }}},
-      &wide, &info);
-  // Threads per workgroup: the largest divisor of both vector counts up to
-  // 256 (whole passes over the tile on either side); at least one wave.
-  const i64 nvg = std::gcd(TILE / VL, TILE / VS);
+  if (contig) block = false;
+  // Threads per workgroup: the largest divisor of both vector (block) counts
+  // up to 256 (whole passes over the tile on either side); at least one wave.
+  const i64 nvg = std::gcd(TILE / (block ? BLK : VL), TILE / VS);
   int NT = 1;
   for (int t = 256; t >= 1; --t)
     if (nvg % t == 0) {
@@ -793,10 +820,206 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   if (NT < 64 && NT != nvg) throw Unsupported("LDS tile does not divide into vectors");
   // each thread holds TILE / NT elements in registers between the two phases
   if (TILE * elem_bytes / NT > 512) throw Unsupported("LDS tile too large for its thread count");
+  // Bank conflicts of one tile under the swizzle stride S, counted on the
+  // host: 32 banks of 4 bytes; an access of A bytes per lane is served 128/A
+  // lanes at a time (all 64 for narrower ones), and a group costs as many
+  // passes as the most distinct dwords any one bank receives in it.  (This
+  // model reproduces the LDS bank-conflict cycles counted on gfx950 for the
+  // scattered and block transfers of transposes and Morton orders.)
+  auto dig = [&](i64 x, i64 weight, i64 b) { return (x / weight) % b; };
+  auto kd_num = [&](i64 ks) {
+    i64 kd = 0;
+    for (size_t k : ts) kd += dig(ks, ws[k], d[k].b) * wd[k];
+    return kd;
+  };
+  // The XOR key of LDS row r: (r / S) % K with K = W / VS (the XOR-swizzle
+  // GenP over [TILE / W, W]), optionally XORed with (r / S2) % K for a second
+  // stride S2 > S (0: none), which separates lanes whose rows differ in bits
+  // that one window of the row index does not cover.
+  i64 swz_s2 = 0;
+  auto key_num = [&](i64 r, i64 S, i64 S2) {
+    const i64 K = W / VS;
+    return ((r / S) % K) ^ (S2 ? (r / S2) % K : 0);
+  };
+  auto slot_num = [&](i64 kd, i64 S, i64 S2) {
+    if (!swz) return kd;
+    const i64 r = kd / W, col = kd % W;
+    return r * W + (((col / VS) ^ key_num(r, S, S2)) * VS) + col % VS;
+  };
+  auto passes = [&](const std::vector<i64>& slot, int bytes) {  // one instruction of one wave
+    const int gsz = (int)std::min<i64>(64, std::max(1, 128 / bytes));
+    i64 total = 0;
+    for (size_t g0 = 0; g0 < slot.size(); g0 += gsz) {
+      std::map<i64, std::set<i64>> bank;
+      for (size_t l = g0; l < std::min(slot.size(), g0 + gsz); ++l)
+        for (i64 dw = slot[l] * elem_bytes / 4; dw <= (slot[l] * elem_bytes + bytes - 1) / 4; ++dw)
+          bank[dw % 32].insert(dw);
+      size_t m = 1;
+      for (auto& kv : bank) m = std::max(m, kv.second.size());
+      total += (i64)m;
+    }
+    return total;
+  };
+  auto conflicts = [&](i64 S, i64 S2, i64* wr, i64* rd) {
+    *wr = *rd = 0;
+    std::vector<i64> sl;
+    const i64 nq = block ? TILE / BLK : TILE / VL;
+    for (i64 q0 = 0; q0 < nq; q0 += 64) {  // one wave's instruction
+      const i64 lanes = std::min<i64>(64, nq - q0);
+      const i64 ninst = block ? NY : (contig ? 1 : VL);
+      for (i64 u = 0; u < ninst; ++u) {
+        sl.clear();
+        for (i64 l = 0; l < lanes; ++l) {
+          const i64 q = q0 + l;
+          i64 kd = 0;
+          if (block) {
+            for (size_t k : bd) kd += dig(q, wb[k], d[k].b) * wd[k];
+            for (size_t k : yd) kd += dig(u, wy[k], d[k].b) * wd[k];
+          } else {
+            kd = kd_num(q * VL + u);
+          }
+          sl.push_back(slot_num(kd, S, S2));
+        }
+        const i64 p = passes(sl, (int)((block ? VS : contig ? VL : 1) * elem_bytes));
+        *wr += p - (lanes + 63) / 64 * std::max<i64>(1, (block ? VS : contig ? VL : 1) * elem_bytes * 64 / 128);
+      }
+    }
+    for (i64 q0 = 0; q0 < TILE / VS; q0 += 64) {
+      sl.clear();
+      for (i64 l = 0; l < std::min<i64>(64, TILE / VS - q0); ++l) sl.push_back(slot_num((q0 + l) * VS, S, S2));
+      *rd += passes(sl, (int)(VS * elem_bytes)) - std::max<i64>(1, VS * elem_bytes * 64 / 128);
+    }
+  };
+  // Candidates: rows of 256 and of 128 bytes (the latter keep two vectors
+  // half a 256-byte row apart, which share banks under any XOR of the row,
+  // in different rows) and every stride S; the fewest passes win.
+  i64 swz_s = contig ? 1 : VL, best_w = 0, best_r = 0;
+  if (swz) {
+    conflicts(swz_s, 0, &best_w, &best_r);
+    const i64 W256 = W;
+    // single strides first (fewer operations), pairs only if still needed
+    for (int pairs = 0; pairs < 2 && best_w + best_r > 0; ++pairs)
+      for (i64 wb : {256, 128}) {
+        const i64 w = row_of(wb);
+        if (!swizzles(w) || (wb == 128 && w == W256)) continue;
+        const i64 keep = W;
+        W = w;
+        bool better = false;
+        for (i64 S = 1; S <= TILE / W; S *= 2)
+          for (i64 S2 = pairs ? 2 * S : 0; S2 <= (pairs ? TILE / W : 0); S2 = S2 ? S2 * 2 : 1) {
+            i64 cw, cr;
+            conflicts(S, S2, &cw, &cr);
+            if (cw + cr < best_w + best_r) swz_s = S, swz_s2 = S2, best_w = cw, best_r = cr, better = true;
+            if (!pairs) break;
+          }
+        if (!better) W = keep;
+      }
+  }
+  swz_s = std::max<i64>(1, tune("remap.swizzle", swz_s));
+  swz_s2 = std::max<i64>(0, tune("remap.swizzle2", swz_s2));
+  W = row_of(tune("remap.lds_row", W * elem_bytes));
+  if (swz) conflicts(swz_s, swz_s2, &best_w, &best_r);
+  auto lds_slot = [&](Ctx& c, const Sum& kd) {
+    if (!swz) return kd;
+    const i64 K = W / VS;
+    Sum r = fdiv(c, kd, W), col = fmod(c, kd, W);
+    Sum key = fmod(c, fdiv(c, r, swz_s), K);
+    if (swz_s2) key = bxor(c, key, fmod(c, fdiv(c, r, swz_s2), K));
+    return add(c, add(c, mulc(c, r, W), mulc(c, bxor(c, fdiv(c, col, VS), key), VS)), fmod(c, col, VS));
+  };
+  auto group_part = [&](Ctx& c, int g, bool dst_side) {
+    Sum o = cst(0);
+    for (size_t k : gd) o = add(c, o, mulc(c, digit_of(c, var(c, g), wg[k], d[k].b), dst_side ? d[k].a : d[k].c));
+    return o;
+  };
+  std::vector<std::pair<std::string, std::function<FnSpec(Ctx&)>>> fnl;
+  if (block) {
+    fnl.push_back({"src_off", [&](Ctx& c) {
+                     int g = c.var("g", G), b = c.var("b", TILE / BLK), x = c.var("x", NX);
+                     Sum o = group_part(c, g, false);
+                     for (size_t k : bd) o = add(c, o, mulc(c, digit_of(c, var(c, b), wb[k], d[k].b), d[k].c));
+                     for (size_t k : xd) o = add(c, o, mulc(c, digit_of(c, var(c, x), wx[k], d[k].b), d[k].c));
+                     FnSpec f;
+                     f.params = {g, b, x};
+                     f.outs = {o};
+                     return f;
+                   }});
+    fnl.push_back({"ldsw", [&](Ctx& c) {
+                     int b = c.var("b", TILE / BLK), y = c.var("y", NY);
+                     Sum kd = cst(0);
+                     for (size_t k : bd) kd = add(c, kd, mulc(c, digit_of(c, var(c, b), wb[k], d[k].b), wd[k]));
+                     for (size_t k : yd) kd = add(c, kd, mulc(c, digit_of(c, var(c, y), wy[k], d[k].b), wd[k]));
+                     FnSpec f;
+                     f.params = {b, y};
+                     f.outs = {lds_slot(c, kd)};
+                     return f;
+                   }});
+  } else {
+    fnl.push_back({"src_off", [&](Ctx& c) {
+                     int g = c.var("g", G), q = c.var("q", TILE / VL);
+                     Sum ks = mulc(c, var(c, q), VL);
+                     Sum o = group_part(c, g, false);
+                     for (size_t k : ts) o = add(c, o, mulc(c, digit_of(c, ks, ws[k], d[k].b), d[k].c));
+                     FnSpec f;
+                     f.params = {g, q};
+                     f.outs = {o};
+                     return f;
+                   }});
+    fnl.push_back({"ldsw", [&](Ctx& c) {
+                     int q = c.var("q", TILE / VL), e = c.var("e", VL);
+                     Sum ks = add(c, mulc(c, var(c, q), VL), var(c, e));
+                     FnSpec f;
+                     f.params = {q, e};
+                     f.outs = {lds_slot(c, kd_from_ks(c, ks))};
+                     return f;
+                   }});
+  }
+  fnl.push_back({"ldsr", [&](Ctx& c) {
+                   int q = c.var("q", TILE / VS);
+                   FnSpec f;
+                   f.params = {q};
+                   f.outs = {lds_slot(c, mulc(c, var(c, q), VS))};
+                   return f;
+                 }});
+  fnl.push_back({"dst_off", [&](Ctx& c) {
+                   int g = c.var("g", G), q = c.var("q", TILE / VS);
+                   Sum kd = mulc(c, var(c, q), VS);
+                   Sum o = group_part(c, g, true);
+                   for (size_t k : td) o = add(c, o, mulc(c, digit_of(c, kd, wd[k], d[k].b), d[k].a));
+                   FnSpec f;
+                   f.params = {g, q};
+                   f.outs = {o};
+                   return f;
+                 }});
+  std::string fns = emit_all(fnl, &wide, &info);
+  // The block's register permutation: element e of destination vector y is
+  // element blk_el(y * VS + e) of the block's loads (source vector x at
+  // x * VL, its element at + e).
+  std::string blk_tab;
+  if (block) {
+    std::ostringstream t;
+    t << "LEGO_FN constexpr int blk_el(int k) {\n  constexpr int t[" << NY * VS << "] = {";
+    for (i64 y = 0; y < NY; ++y)
+      for (i64 e = 0; e < VS; ++e) {
+        // digit values of this element: Y digits from y, destination-vector digits from e
+        std::vector<i64> val(d.size(), 0);
+        for (size_t k : yd) val[k] = dig(y, wy[k], d[k].b);
+        for (size_t k : td)
+          if (in_vs[k]) val[k] = dig(e, wd[k], d[k].b);
+        i64 x = 0, el = 0;
+        for (size_t k : xd) x += val[k] * wx[k];
+        for (size_t k : ts)
+          if (in_vl[k]) el += val[k] * ws[k];
+        t << (y || e ? ", " : "") << x * VL + el;
+      }
+    t << "};\n  return t[k];\n}\n";
+    blk_tab = t.str();
+  }
   s << header() << "#define ELEM_T " << et << "\n#define IDX_T " << (wide ? "i64" : "u32") << "\n#define TILE " << TILE
     << "\n#define NELEM " << N << "ull\n#define NTILES " << G << "ull\n#define NT " << NT << "\n#define VL " << VL << "\n#define VS " << VS << "\n#define LDSW_CONTIG "
-    << (contig ? 1 : 0) << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_LDS 1\n"
-    << fns << "// ---- template ----\n" << tpl_remap;
+    << (contig ? 1 : 0) << "\n#define LDS_BLOCK " << (block ? 1 : 0) << "\n#define NX " << NX << "\n#define NY " << NY
+    << "\n#define NONTEMPORAL " << nontemporal << "\n#define LEGO_REMAP_LDS 1\n"
+    << fns << blk_tab << "// ---- template ----\n" << tpl_remap;
   R.kernel = "lego_remap_lds";
   R.block = NT;
   R.grid = G;
@@ -805,7 +1028,9 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   R.tile = TILE;
   R.src = s.str();
   R.info = "lds TILE=" + std::to_string(TILE) + " VL=" + std::to_string(VL) + " VS=" + std::to_string(VS) +
-           " W=" + std::to_string(W) + (swz ? " xor" : " row") + (contig ? " contig" : " scatter") +
+           " W=" + std::to_string(W) + (swz ? " xor/" + std::to_string(swz_s) + (swz_s2 ? "^" + std::to_string(swz_s2) : "") : " row") +
+           (block ? " block " + std::to_string(NX) + "x" + std::to_string(NY) : contig ? " contig" : " scatter") +
+           " bank-passes+" + std::to_string(best_w) + "/" + std::to_string(best_r) +
            (lds_src_order ? " src-order" : " dst-order") +
            " run=" + std::to_string(run) + info;
   return R;

@@ -184,6 +184,22 @@ def test_plans_choose_expected_paths(lego):
     assert "waves 2x2 wave 128x128" in info
 
 
+def test_lds_plans_transfer_blocks_without_bank_conflicts(lego):
+    """Transposing tiles move whole blocks (a thread's loads hold whole
+    destination vectors, permuted in registers), and the planner's count of
+    LDS bank passes over one tile finds none beyond the minimum for the
+    transposes and the row -> Morton remap.  Morton -> row keeps scattered
+    element writes: its destination vectors would need loads with gaps."""
+    L = lego
+    for n, eb in ((2048, 4), (4096, 4), (8192, 4), (4096, 2), (1024, 2)):
+        info = L.remap_plan(L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n)), eb)["info"]
+        assert " block " in info and " bank-passes+0/0 " in info, (n, eb, info)
+    row, mz = L.as_layout(L.Row(4096, 4096)), L.as_layout(L.GenP("morton", [4096, 4096]))
+    info = L.remap_plan(row, mz, 2)["info"]
+    assert " block 2x2 " in info and " bank-passes+0/0 " in info, info
+    assert " scatter " in L.remap_plan(mz, row, 2)["info"]
+
+
 def test_binding_checks_buffer_sizes_before_launch(lego):
     """The binding refuses buffers smaller than a layout's physical size
     (checked on the host, before any device call)."""

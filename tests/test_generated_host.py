@@ -134,7 +134,12 @@ int main(int argc, char** argv) {
   }
 #else
   const u64 n = NELEM, nsrc = NELEM;
+#if LDS_BLOCK
+  if (NT < 1 || NT > 256 || (TILE / (VL * NX)) % NT || (TILE / VS) % NT) FAIL("NT does not divide the tile's blocks");
+  if (VL * NX != VS * NY) FAIL("a block holds NX source and NY destination vectors");
+#else
   if (NT < 1 || NT > 256 || (TILE / VL) % NT || (TILE / VS) % NT) FAIL("NT does not divide the tile's vectors");
+#endif
   if ((unsigned long long)TILE * sizeof(ELEM_T) > 131072) FAIL("LDS tile exceeds 128 KiB");
   if ((unsigned long long)TILE * sizeof(ELEM_T) / NT > 512) FAIL("too many tile elements per thread");
   std::vector<long long> perm(n, -2);
@@ -142,6 +147,27 @@ int main(int argc, char** argv) {
   std::vector<char> wseen(TILE);
   for (u64 g = 0; g < NTILES; ++g) {
     std::fill(tile.begin(), tile.end(), -1);
+#if LDS_BLOCK
+    for (u64 b = 0; b < TILE / (VL * NX); ++b) {
+      long long blk[VL * NX];
+      for (u64 x = 0; x < NX; ++x) {
+        u64 s = (u64)src_off((IDX_T)g, (IDX_T)b, (IDX_T)x);
+        if (s % VL || s + VL > n) FAIL("src_off(%llu,%llu,%llu) = %llu bad", (unsigned long long)g, (unsigned long long)b, (unsigned long long)x, (unsigned long long)s);
+        for (int e = 0; e < VL; ++e) blk[x * VL + e] = (long long)(s + e);
+      }
+      std::vector<char> used(VL * NX);
+      for (u64 y = 0; y < NY; ++y) {
+        u64 l = (u64)ldsw((IDX_T)b, (IDX_T)y);
+        if (l % VS || l + VS > TILE) FAIL("ldsw out of range or misaligned");
+        for (int e = 0; e < VS; ++e) {
+          const int k = blk_el((int)(y * VS + e));
+          if (k < 0 || k >= VL * NX || used[k]++) FAIL("blk_el is not a permutation of the block");
+          if (g == 0) { if (wseen[l + e]++) FAIL("ldsw not injective"); }
+          tile[l + e] = blk[k];
+        }
+      }
+    }
+#else
     for (u64 q = 0; q < TILE / VL; ++q) {
       u64 s = (u64)src_off((IDX_T)g, (IDX_T)q);
       if (s % VL || s + VL > n) FAIL("src_off(%llu,%llu) = %llu bad", (unsigned long long)g, (unsigned long long)q, (unsigned long long)s);
@@ -152,6 +178,7 @@ int main(int argc, char** argv) {
         tile[l] = (long long)(s + e);
       }
     }
+#endif
     for (u64 q = 0; q < TILE / VS; ++q) {
       u64 l = (u64)ldsr((IDX_T)q);
       u64 d = (u64)dst_off((IDX_T)g, (IDX_T)q);
@@ -207,14 +234,28 @@ int main() {
   if (!rd.all(NSRC / V) || !wr.all(NVEC)) FAIL("element never copied");
 #else
   const u64 n = NELEM;
+#if LDS_BLOCK
+  if (NT < 1 || NT > 256 || (TILE / (VL * NX)) % NT || (TILE / VS) % NT) FAIL("NT does not divide the tile's blocks");
+  if (VL * NX != VS * NY) FAIL("a block holds NX source and NY destination vectors");
+#else
   if (NT < 1 || NT > 256 || (TILE / VL) % NT || (TILE / VS) % NT) FAIL("NT does not divide the tile's vectors");
+#endif
   Bits rd(n / VL), wr(n / VS);
   for (u64 g = 0; g < NTILES; ++g) {
+#if LDS_BLOCK
+    for (u64 b = 0; b < TILE / (VL * NX); ++b)
+      for (u64 x = 0; x < NX; ++x) {
+        u64 s = (u64)src_off((IDX_T)g, (IDX_T)b, (IDX_T)x);
+        if (s % VL || s + VL > n) FAIL("src_off out of range");
+        if (rd.set(s / VL)) FAIL("source read twice");
+      }
+#else
     for (u64 q = 0; q < TILE / VL; ++q) {
       u64 s = (u64)src_off((IDX_T)g, (IDX_T)q);
       if (s % VL || s + VL > n) FAIL("src_off out of range");
       if (rd.set(s / VL)) FAIL("source read twice");
     }
+#endif
     for (u64 q = 0; q < TILE / VS; ++q) {
       u64 d = (u64)dst_off((IDX_T)g, (IDX_T)q);
       if (d % VS || d + VS > n) FAIL("dst_off out of range");
