@@ -513,7 +513,8 @@ def _remap_pair(L, name):
 WORKLOADS = ("remap: blocked_f32_8192, transpose_f32_{2048,4096,8192}, morton_f16_4096, antidiag_f32_{4096,8192}, "
              "identity_f32_8192 (a plain copy) "
              "(suffix _fwd or _inv: one direction only, its source fixed; _flushed: a 1 GiB fill evicts the "
-             "last-level cache before each launch); gemm: gemm_bf16_8192, gemm_morton_f16_4096")
+             "last-level cache before each launch); gemm: gemm_bf16_8192 (the measured GEMM), "
+             "gemm_<f16|bf16>_<n>_<A>_<B> with A, B each row, col or morton")
 
 
 def run_workload(L, name, reps):
@@ -526,16 +527,24 @@ def run_workload(L, name, reps):
         g = bench_gemm(L, reps, 30)
         return {"workload": name, "ms": round(g["ms"], 5), "tflops": round(g["tflops"], 1), "plan": g["plan"]}
     if name.startswith("gemm_"):
-        dt, n = name.split("_")[2], int(name.split("_")[3])
+        # gemm_<dtype>_<n>_<A>_<B>, A and B each row, col or morton
+        _, dt, n, la, lb = name.split("_")
+        n = int(n)
         a = S.tensor(n * n, dt, dist="normal", seed=S.SEED_A).cuda()
         b = S.tensor(n * n, dt, dist="normal", seed=S.SEED_B).cuda()
         c = torch.empty(n * n, dtype=torch.float32, device="cuda")
-        kw = {}
-        if "morton" in name:
-            mz = L.as_layout(L.GenP("morton", [n, n]))
-            a_mz = torch.empty_like(a)
-            L.remap(L.as_layout(L.Row(n, n)), mz, a, a_mz)
-            a, kw = a_mz, dict(a=mz, b=L.as_layout(L.Row(n, n)))
+        lay = {"row": lambda: L.as_layout(L.Row(n, n)), "col": lambda: L.as_layout(L.Col(n, n)),
+               "morton": lambda: L.as_layout(L.GenP("morton", [n, n]))}
+        kw = dict(a=lay[la](), b=lay[lb]())
+        # the operands' values are those of a row-major matrix, stored in each layout
+        if la != "row":
+            t = torch.empty_like(a)
+            L.remap(lay["row"](), kw["a"], a, t)
+            a = t
+        if lb != "row":
+            t = torch.empty_like(b)
+            L.remap(lay["row"](), kw["b"], b, t)
+            b = t
         ms = _gemm_ms(L, a, b, c, n, dt, reps, warmup=10, **kw)
         return {"workload": name, "ms": round(ms, 5), "tflops": round(2.0 * n ** 3 / ms / 1e9, 1),
                 "plan": L.gemm_plan(n, n, n, dt, **kw)}

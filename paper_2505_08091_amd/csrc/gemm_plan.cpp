@@ -811,7 +811,11 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // A persistent grid walks several tiles per workgroup, chaining the LDS
   // ring across tiles: the first steps of the next tile are requested during
   // the last NSTAGES steps of the current one, so a tile needs that many.
-  const bool persist = direct && Kt >= nstages && tune("gemm.persist", 1) != 0;
+  // Not for padded tiles with at most one tile per compute unit (256 on
+  // gfx950): there the walk gains nothing and its state pushes the range
+  // checks' registers into spills (513x257x320 fp16: 53 VGPRs).
+  const bool persist = direct && Kt >= nstages && !((ops[0].edge || ops[1].edge || cedge) && P <= 256) &&
+                       tune("gemm.persist", 1) != 0;
   s << "#define C_SEP " << (csep ? 1 : 0) << "\n#define PERSIST " << (persist ? 1 : 0) << "\n" << code << "// ---- template ----\n" << tpl_gemm;
 
   GemmPlan g;
@@ -836,20 +840,23 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
        << (ops[0].edge || ops[1].edge || cedge ? " edges" : "") << (persist ? " persistent" : "") << " stages " << nstages << " lds " << nstages * stage_bytes
        << "B ops" << opsinfo.str();
   g.info = info.str();
-  g.direct_vec = direct && ops[0].frvec && ops[1].frvec;
+  g.wide_ok = direct && !(ops[0].edge || ops[1].edge || cedge);
   return g;
 }
 
 }  // namespace
 
 GemmPlan plan_gemm(const GemmRequest& rq) {
-  // 128x128 wave tiles (4 waves) win where the copies are direct and the
-  // fragments are read as vectors: 0.852 against 0.876 ms for 8 waves of
-  // 128x64 on the 8192^3 bf16 GEMM, reading 1/3 less LDS per MFMA.  Otherwise
-  // two waves per SIMD do better (register-staged 4096^3 Morton-A GEMM: 913-922
-  // TFLOP/s with 8 waves, 850 with 4; transposing fragment reads: ~3%).
+  // 128x128 wave tiles (4 waves) win where the copies are direct: 0.852
+  // against 0.876 ms for 8 waves of 128x64 on the 8192^3 bf16 GEMM, reading
+  // 1/3 less LDS per MFMA, and 1-5% with transposing fragment reads (8192^3
+  // fp16 A row-major, B row-major: 1241-1248 -> 1264-1269 TFLOP/s; A column-
+  // major: 1215-1219 -> 1244-1254).  Register-staged plans keep two waves per
+  // SIMD (4096^3 Morton-A GEMM: 908-937 TFLOP/s with 8 waves, 833-872 with
+  // 4), and so do plans with padded tiles, whose range checks need more
+  // registers than one wave per SIMD leaves (1000^3 bf16: 177 VGPRs spilled).
   GemmPlan p = plan_gemm_waves(rq, true);
-  if (rq.wn || p.direct_vec) return p;
+  if (rq.wn || p.wide_ok) return p;
   return plan_gemm_waves(rq, false);
 }
 
@@ -938,6 +945,14 @@ std::vector<std::pair<std::string, std::string>> selftest_sources() {
     g6.xcd = 1;
     out.push_back({both ? "gemm 4096^3 f16 col A, row B" : "gemm 4096^3 f16 row A, row B", plan_gemm(g6).src});
   }
+  // Transposing reads with padded tiles (1000 = 3 * 256 + 232).
+  GemmRequest g7;
+  g7.M = g7.N = g7.K = 1000;
+  g7.dtype = LEGO_F16;
+  g7.a = make_from_piece(make_col({1000, 1000}));
+  g7.b = make_from_piece(make_row({1000, 1000}));
+  g7.xcd = 1;
+  out.push_back({"gemm 1000^3 f16 col A, row B, padded tiles", plan_gemm(g7).src});
   return out;
 }
 

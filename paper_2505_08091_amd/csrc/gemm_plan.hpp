@@ -24,7 +24,9 @@ struct GemmRequest {
 };
 
 struct GemmPlan : KernelPlan {
-  bool direct_vec = false;  // direct copies, both operands' fragments read as vectors
+  // direct global-to-LDS copies whose 128x128 wave tiles fit the registers
+  // (not with padded tiles: their range checks spill with one wave per SIMD)
+  bool wide_ok = false;
 };
 
 GemmRequest gemm_request(const lego_gemm_desc& d, const std::function<LayoutP(lego_layout_t)>& resolve);

@@ -640,6 +640,11 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         kstep((int)((stage0 + kt) % NSTAGES), own ? cur : nxt, (kt + NSTAGES) % KT);
       }
     }
+    // After the workgroup's last tile the fragment reads issued by the last
+    // step are dead, and the epilogue may reuse their registers: wait for
+    // them first (between tiles they hold the next tile's fragments, which
+    // stay live across the epilogue).
+    if (!has_next) FRAG_WAIT();
     store_c(cur.tm, cur.tn);
     if (!has_next) break;
 #pragma unroll

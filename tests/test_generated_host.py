@@ -446,7 +446,7 @@ def _compile_and_run(src, harness, tmp, args=()):
     return r.stdout
 
 
-N_SOURCES = 15
+N_SOURCES = 16
 
 
 def test_source_count():

@@ -328,7 +328,7 @@ def _persistent_cases(L):
         dict(M=1024, N=512, K=1024, dtype="bf16", max_workgroups=3),
         dict(M=1024, N=768, K=320, dtype="f16", max_workgroups=5),
         dict(M=1024, N=512, K=1024, dtype="bf16", bk=32, stages=4, max_workgroups=3),
-        dict(M=1000, N=1000, K=1000, dtype="bf16", max_workgroups=7),
+        dict(M=4100, N=4100, K=136, dtype="bf16", max_workgroups=7),
         dict(M=1024, N=512, K=1024, dtype="f16", a=L.as_layout(L.Col(1024, 1024)), b=L.as_layout(L.Row(1024, 512)),
              oa=OL.as_layout(OL.Col(1024, 1024)), ob=OL.as_layout(OL.Row(1024, 512)), max_workgroups=3),
         dict(M=1024, N=512, K=512, dtype="bf16", max_workgroups=1),

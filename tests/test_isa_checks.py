@@ -138,6 +138,21 @@ def test_checker_finds_a_planted_early_use():
     assert untracked_load_violations(parse(ok)) == []
 
 
+def test_generated_kernels_do_not_spill(dumped):
+    """No generated kernel of the built-in configurations spills registers to
+    scratch memory (a spill store of a transposing read's destination would
+    also read it before its wait)."""
+    readelf = os.path.join(os.path.dirname(OBJDUMP), "llvm-readelf")
+    n = 0
+    for co in sorted(dumped.glob("*.co")):
+        notes = subprocess.run([readelf, "--notes", str(co)], capture_output=True, text=True, check=True).stdout
+        spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", notes)]
+        spills += [int(x) for x in re.findall(r"\.sgpr_spill_count:\s+(\d+)", notes)]
+        assert spills and not any(spills), (co.name, spills)
+        n += 1
+    assert n >= 10
+
+
 def test_transposing_fragment_reads_are_waited_for(dumped):
     n = 0
     for hip in sorted(dumped.glob("*.hip")):
@@ -153,3 +168,42 @@ def test_transposing_fragment_reads_are_waited_for(dumped):
         assert not bad, (hip.name, bad[:5])
         n += 1
     assert n >= 2  # the built-in configurations with m- and n-contiguous operands
+
+
+HIPCC = "/opt/rocm/bin/hipcc"
+BUNDLER = "/opt/rocm/llvm/bin/clang-offload-bundler"
+
+
+def _gemm_case_ids():
+    from tests.test_generated_host import N_GEMM_CASES
+    return range(N_GEMM_CASES)
+
+
+@pytest.mark.parametrize("i", _gemm_case_ids())
+def test_gemm_configurations_of_the_gpu_tests_compile_clean(i, tmp_path):
+    """Every GEMM configuration the GPU tests launch, compiled for gfx950 with
+    the library's compiler options: no register spills, and no transposing
+    read's destination touched before its wait."""
+    if not (os.path.exists(HIPCC) and os.path.exists(BUNDLER) and os.path.exists(OBJDUMP)):
+        pytest.skip("no ROCm compiler")
+    import paper_2505_08091_amd as L
+    from tests.test_generated_host import _gemm_cases
+    kw = dict(_gemm_cases()[i])
+    src = L.plan_source("gemm", **kw)
+    hip, co, elf = tmp_path / "k.hip", tmp_path / "k.co", tmp_path / "k.elf"
+    hip.write_text(src)
+    r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "--genco", "-Xclang", "-target-feature",
+                        "-Xclang", "-packed-fp32-ops", "-include", "hip/hip_runtime.h", str(hip), "-o", str(co)],
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode == 0, r.stderr[-2000:]
+    subprocess.run([BUNDLER, "--unbundle", "--type=o", "--targets=hipv4-amdgcn-amd-amdhsa--gfx950",
+                    f"--input={co}", f"--output={elf}"], check=True, capture_output=True)
+    readelf = os.path.join(os.path.dirname(OBJDUMP), "llvm-readelf")
+    notes = subprocess.run([readelf, "--notes", str(elf)], capture_output=True, text=True, check=True).stdout
+    spills = [int(x) for x in re.findall(r"\.[vs]gpr_spill_count:\s+(\d+)", notes)]
+    assert spills and not any(spills), (kw, spills)
+    if "#define A_FRTR 1" in src or "#define B_FRTR 1" in src:
+        text = subprocess.run([OBJDUMP, "-d", "--mcpu=gfx950", str(elf)], capture_output=True, text=True,
+                              check=True).stdout
+        bad = untracked_load_violations(parse(text))
+        assert not bad, (kw, bad[:5])
