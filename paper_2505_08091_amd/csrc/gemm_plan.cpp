@@ -811,10 +811,10 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // A persistent grid walks several tiles per workgroup, chaining the LDS
   // ring across tiles: the first steps of the next tile are requested during
   // the last NSTAGES steps of the current one, so a tile needs that many.
-  // Not for padded tiles with at most one tile per compute unit (256 on
-  // gfx950): there the walk gains nothing and its state pushes the range
-  // checks' registers into spills (513x257x320 fp16: 53 VGPRs).
-  const bool persist = direct && Kt >= nstages && !((ops[0].edge || ops[1].edge || cedge) && P <= 256) &&
+  // Not with padded tiles: the range checks of two tiles' copies do not fit
+  // the registers beside the walk's state (8000^3 bf16: 240 VGPRs spilled
+  // with 8 waves, 613 with 4; none without the walk).
+  const bool persist = direct && Kt >= nstages && !(ops[0].edge || ops[1].edge || cedge) &&
                        tune("gemm.persist", 1) != 0;
   s << "#define C_SEP " << (csep ? 1 : 0) << "\n#define PERSIST " << (persist ? 1 : 0) << "\n" << code << "// ---- template ----\n" << tpl_gemm;
 
@@ -840,7 +840,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
        << (ops[0].edge || ops[1].edge || cedge ? " edges" : "") << (persist ? " persistent" : "") << " stages " << nstages << " lds " << nstages * stage_bytes
        << "B ops" << opsinfo.str();
   g.info = info.str();
-  g.wide_ok = direct && !(ops[0].edge || ops[1].edge || cedge);
+  g.wide_ok = direct && !((ops[0].frtr || ops[1].frtr) && (ops[0].edge || ops[1].edge || cedge));
   return g;
 }
 
@@ -853,10 +853,11 @@ GemmPlan plan_gemm(const GemmRequest& rq) {
   // fp16 A row-major, B row-major: 1241-1248 -> 1264-1269 TFLOP/s; A column-
   // major: 1215-1219 -> 1244-1254).  Register-staged plans keep two waves per
   // SIMD (4096^3 Morton-A GEMM: 908-937 TFLOP/s with 8 waves, 833-872 with
-  // 4), and so do plans with padded tiles, whose range checks need more
-  // registers than one wave per SIMD leaves (1000^3 bf16: 177 VGPRs spilled).
+  // 4), and so do plans with transposing reads and padded tiles (1000^3
+  // fp16, A column-major: 176 VGPRs spilled with 4 waves).
   GemmPlan p = plan_gemm_waves(rq, true);
-  if (rq.wn || p.wide_ok) return p;
+  const long long wide = tune("gemm.wide_waves", -1);  // -1: the rule above
+  if (rq.wn || (wide < 0 ? p.wide_ok : wide != 0)) return p;
   return plan_gemm_waves(rq, false);
 }
 

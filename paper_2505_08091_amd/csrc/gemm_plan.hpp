@@ -25,7 +25,7 @@ struct GemmRequest {
 
 struct GemmPlan : KernelPlan {
   // direct global-to-LDS copies whose 128x128 wave tiles fit the registers
-  // (not with padded tiles: their range checks spill with one wave per SIMD)
+  // (not transposing reads with padded tiles)
   bool wide_ok = false;
 };
 

@@ -591,7 +591,7 @@ def _gemm_cases():
     return cases
 
 
-N_GEMM_CASES = 42
+N_GEMM_CASES = 41
 
 
 def test_gemm_case_count():

@@ -322,20 +322,20 @@ def _persistent_cases(L):
     persistent and max_workgroups is below the tile count), so the LDS ring
     chains from one tile into the next: uneven tile counts per workgroup,
     k-step counts that do not divide by the stage count (the ring's first
-    stage alternates between tiles), four 32-deep stages, partial tiles, the
-    transposing fragment reads, and a single workgroup doing everything."""
+    stage alternates between tiles), four 32-deep stages, the transposing
+    fragment reads, and a single workgroup doing everything (plans with
+    partial tiles do not walk)."""
     return [
         dict(M=1024, N=512, K=1024, dtype="bf16", max_workgroups=3),
         dict(M=1024, N=768, K=320, dtype="f16", max_workgroups=5),
         dict(M=1024, N=512, K=1024, dtype="bf16", bk=32, stages=4, max_workgroups=3),
-        dict(M=4100, N=4100, K=136, dtype="bf16", max_workgroups=7),
         dict(M=1024, N=512, K=1024, dtype="f16", a=L.as_layout(L.Col(1024, 1024)), b=L.as_layout(L.Row(1024, 512)),
              oa=OL.as_layout(OL.Col(1024, 1024)), ob=OL.as_layout(OL.Row(1024, 512)), max_workgroups=3),
         dict(M=1024, N=512, K=512, dtype="bf16", max_workgroups=1),
     ]
 
 
-@pytest.mark.parametrize("i", range(6))
+@pytest.mark.parametrize("i", range(5))
 def test_gemm_persistent_tile_walk(lego, i):
     kw = dict(_persistent_cases(lego)[i])
     M, N, K, dtype = kw.pop("M"), kw.pop("N"), kw.pop("K"), kw.pop("dtype")

@@ -176,19 +176,34 @@ BUNDLER = "/opt/rocm/llvm/bin/clang-offload-bundler"
 
 def _gemm_case_ids():
     from tests.test_generated_host import N_GEMM_CASES
-    return range(N_GEMM_CASES)
+    return range(N_GEMM_CASES + len(_measured_gemms(None)))
+
+
+def _measured_gemms(L):
+    """The measured GEMMs that the GPU tests do not launch at these sizes."""
+    if L is None:
+        return [None] * 6
+    n = 8192
+    out = [dict(M=8000, N=8000, K=8000, dtype="bf16")]
+    for la in ("Row", "Col"):
+        for lb in ("Row", "Col"):
+            out.append(dict(M=n, N=n, K=n, dtype="f16", a=L.as_layout(getattr(L, la)(n, n)),
+                            b=L.as_layout(getattr(L, lb)(n, n))))
+    out.append(dict(M=1024, N=1024, K=1024, dtype="f16", bm=128, bn=128, bk=32, wm=64, wn=64))
+    return out
 
 
 @pytest.mark.parametrize("i", _gemm_case_ids())
-def test_gemm_configurations_of_the_gpu_tests_compile_clean(i, tmp_path):
-    """Every GEMM configuration the GPU tests launch, compiled for gfx950 with
-    the library's compiler options: no register spills, and no transposing
-    read's destination touched before its wait."""
+def test_gemm_configurations_compile_clean(i, tmp_path):
+    """Every GEMM configuration the GPU tests launch, and the measured ones,
+    compiled for gfx950 with the library's compiler options: no register
+    spills, and no transposing read's destination touched before its wait."""
     if not (os.path.exists(HIPCC) and os.path.exists(BUNDLER) and os.path.exists(OBJDUMP)):
         pytest.skip("no ROCm compiler")
     import paper_2505_08091_amd as L
     from tests.test_generated_host import _gemm_cases
-    kw = dict(_gemm_cases()[i])
+    cases = _gemm_cases() + _measured_gemms(L)
+    kw = dict(cases[i])
     src = L.plan_source("gemm", **kw)
     hip, co, elf = tmp_path / "k.hip", tmp_path / "k.co", tmp_path / "k.elf"
     hip.write_text(src)
