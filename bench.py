@@ -229,6 +229,23 @@ def _alternate(L, la, lb, x, y, z, reps, warmup=5):
     return f, i
 
 
+def _alone(L, la, lb, x, y, reps, warmup=5):
+    """Mean ms of the remap la->lb (x -> y) launched `reps` times in a row."""
+    import torch
+    for _ in range(warmup):
+        L.remap(la, lb, x, y)
+    ev = HipEvents(reps + 1, _stream())
+    torch.cuda.synchronize()
+    for k in range(reps):
+        ev.record(k)
+        L.remap(la, lb, x, y)
+    ev.record(reps)
+    torch.cuda.synchronize()
+    ms = ev.ms(0, reps) / reps
+    ev.close()
+    return ms
+
+
 def _flushed(L, la, lb, x, y, z, scratch, reps):
     """Like _alternate, but a 1 GiB fill (not timed) evicts the 256 MB
     last-level cache before every launch."""
@@ -332,10 +349,16 @@ def bench_extra(L, reps=20):
         x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()
         y, z = torch.empty_like(x), torch.empty_like(x)
         row, col = L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n))
-        f, i = _alternate(L, row, col, x, y, z, reps)
+        # each direction launched repeatedly on its own source; then the two
+        # alternating (each launch then follows one of the other direction,
+        # which at 2048^2 slows the row -> column kernel itself: equal bytes)
+        f = _alone(L, row, col, x, y, reps)
+        i = _alone(L, col, row, y, z, reps)
+        fa, ia = _alternate(L, row, col, x, y, z, reps)
         nb = 2 * n * n * 4
         tr.append({"n": n, "bytes_per_launch": nb, "row_to_col_GBps": gbps(nb, f), "col_to_row_GBps": gbps(nb, i),
                    "frac_hbm": round(2 * nb / ((f + i) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                   "alternating_row_to_col_GBps": gbps(nb, fa), "alternating_col_to_row_GBps": gbps(nb, ia),
                    "plan": L.remap_plan(row, col, 4)["info"]})
         del x, y, z
     out["transpose_f32"] = tr
@@ -558,17 +581,7 @@ def run_workload(L, name, reps):
         if name.endswith("_inv"):
             L.remap(row, other, x, z)
             x, z = z, x
-        for _ in range(5):
-            L.remap(la, lb, x, y)
-        ev = HipEvents(reps + 1, _stream())
-        torch.cuda.synchronize()
-        for k in range(reps):
-            ev.record(k)
-            L.remap(la, lb, x, y)
-        ev.record(reps)
-        torch.cuda.synchronize()
-        ms = ev.ms(0, reps) / reps
-        ev.close()
+        ms = _alone(L, la, lb, x, y, reps)
         return {"workload": name, "ms": round(ms, 5), "GBps": round(nb / ms / 1e6, 1),
                 "plan": L.remap_plan(la, lb, x.element_size())["info"]}
     if name.endswith("_flushed"):
