@@ -349,16 +349,19 @@ def bench_extra(L, reps=20):
         x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()
         y, z = torch.empty_like(x), torch.empty_like(x)
         row, col = L.as_layout(L.Row(n, n)), L.as_layout(L.Col(n, n))
-        # each direction launched repeatedly on its own source; then the two
-        # alternating (each launch then follows one of the other direction,
-        # which at 2048^2 slows the row -> column kernel itself: equal bytes)
-        f = _alone(L, row, col, x, y, reps)
-        i = _alone(L, col, row, y, z, reps)
-        fa, ia = _alternate(L, row, col, x, y, z, reps)
+        # the two directions alternating (each reads the other's output, as
+        # a round trip does), and each launched repeatedly on its own source:
+        # the caches treat the two patterns differently (at 2048^2 the row ->
+        # column kernel that follows a column -> row launch runs twice as
+        # long, equal bytes; at 8192^2 a repeated source stays partly in the
+        # 256 MB last-level cache)
+        f, i = _alternate(L, row, col, x, y, z, reps)
+        fa = _alone(L, row, col, x, y, reps)
+        ia = _alone(L, col, row, y, z, reps)
         nb = 2 * n * n * 4
         tr.append({"n": n, "bytes_per_launch": nb, "row_to_col_GBps": gbps(nb, f), "col_to_row_GBps": gbps(nb, i),
                    "frac_hbm": round(2 * nb / ((f + i) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
-                   "alternating_row_to_col_GBps": gbps(nb, fa), "alternating_col_to_row_GBps": gbps(nb, ia),
+                   "alone_row_to_col_GBps": gbps(nb, fa), "alone_col_to_row_GBps": gbps(nb, ia),
                    "plan": L.remap_plan(row, col, 4)["info"]})
         del x, y, z
     out["transpose_f32"] = tr
