@@ -454,19 +454,20 @@ def bench_extra(L, reps=20):
                                     "plan": L.gemm_plan(n, n, n, "bf16")}
     del a, b, c
 
-    # A whole 4096^2 fp32 matrix in antidiagonal order (Figure 7's GenP, the
-    # wavefront order of Section V's NW example) and back: no digit structure,
-    # so an element gather.
-    n = 4096
-    x = S.tensor(n * n, "f32", seed=S.SEED_SRC).cuda()
-    y, z = torch.empty_like(x), torch.empty_like(x)
-    row, ad = L.as_layout(L.Row(n, n)), L.as_layout(L.GenP("antidiag", [n, n]))
-    f, i = _alternate(L, row, ad, x, y, z, reps)
-    nb = 2 * n * n * 4
-    out["antidiagonal_f32_4096"] = {"bytes_per_launch": nb, "row_to_antidiag_GBps": gbps(nb, f),
-                                    "antidiag_to_row_GBps": gbps(nb, i),
-                                    "plan": L.remap_plan(row, ad, 4)["info"]}
-    del x, y, z
+    # A whole matrix in antidiagonal order (Figure 7's GenP, the wavefront
+    # order of Section V's NW example) and back: no digit structure, so the
+    # box path (square boxes of the index space through LDS).
+    for n, dt in ((4096, "f32"), (8192, "f32"), (4096, "f16")):
+        x = S.tensor(n * n, dt, seed=S.SEED_SRC).cuda()
+        y, z = torch.empty_like(x), torch.empty_like(x)
+        row, ad = L.as_layout(L.Row(n, n)), L.as_layout(L.GenP("antidiag", [n, n]))
+        f, i = _alternate(L, row, ad, x, y, z, reps)
+        nb = 2 * n * n * x.element_size()
+        out[f"antidiagonal_{dt}_{n}"] = {"bytes_per_launch": nb, "row_to_antidiag_GBps": gbps(nb, f),
+                                         "antidiag_to_row_GBps": gbps(nb, i),
+                                         "frac_hbm": round(2 * nb / ((f + i) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                         "plan": L.remap_plan(row, ad, x.element_size())["info"]}
+        del x, y, z
 
     # 3-D bricks (the stencil data layout of Section V): a 512^3 fp32 grid
     # between row-major order and bricks of 8^3 or 4^3 elements stored
