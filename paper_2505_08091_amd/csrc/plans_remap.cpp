@@ -830,12 +830,14 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   if (NT < 64 && NT != nvg) throw Unsupported("LDS tile does not divide into vectors");
   // each thread holds TILE / NT elements in registers between the two phases
   if (TILE * elem_bytes / NT > 512) throw Unsupported("LDS tile too large for its thread count");
-  // Bank conflicts of one tile under the swizzle stride S, counted on the
-  // host: 32 banks of 4 bytes; an access of A bytes per lane is served 128/A
-  // lanes at a time (all 64 for narrower ones), and a group costs as many
-  // passes as the most distinct dwords any one bank receives in it.  (This
-  // model reproduces the LDS bank-conflict cycles counted on gfx950 for the
-  // scattered and block transfers of transposes and Morton orders.)
+  // Bank conflicts of one tile under the swizzle strides, counted on the
+  // host: a write of A bytes per lane is served 128/A lanes at a time over 32
+  // banks of 4 bytes, a read 256/A lanes at a time over 64 banks (all 64
+  // lanes for narrower accesses), and a group costs as many passes as the
+  // most distinct dwords any one bank receives in it.  (The write rule
+  // reproduces the LDS bank-conflict cycles counted on gfx950 for the
+  // scattered and block writes of transposes and Morton orders, the read
+  // rule the conflict-free 16-byte fragment reads of the GEMM.)
   auto dig = [&](i64 x, i64 weight, i64 b) { return (x / weight) % b; };
   auto kd_num = [&](i64 ks) {
     i64 kd = 0;
@@ -856,14 +858,15 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
     const i64 r = kd / W, col = kd % W;
     return r * W + (((col / VS) ^ key_num(r, S, S2)) * VS) + col % VS;
   };
-  auto passes = [&](const std::vector<i64>& slot, int bytes) {  // one instruction of one wave
-    const int gsz = (int)std::min<i64>(64, std::max(1, 128 / bytes));
+  auto passes = [&](const std::vector<i64>& slot, int bytes, bool read) {  // one instruction of one wave
+    const int window = read ? 256 : 128;
+    const int gsz = (int)std::min<i64>(64, std::max(1, window / bytes));
     i64 total = 0;
     for (size_t g0 = 0; g0 < slot.size(); g0 += gsz) {
       std::map<i64, std::set<i64>> bank;
       for (size_t l = g0; l < std::min(slot.size(), g0 + gsz); ++l)
         for (i64 dw = slot[l] * elem_bytes / 4; dw <= (slot[l] * elem_bytes + bytes - 1) / 4; ++dw)
-          bank[dw % 32].insert(dw);
+          bank[dw % (window / 4)].insert(dw);
       size_t m = 1;
       for (auto& kv : bank) m = std::max(m, kv.second.size());
       total += (i64)m;
@@ -890,14 +893,14 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
           }
           sl.push_back(slot_num(kd, S, S2));
         }
-        const i64 p = passes(sl, (int)((block ? VS : contig ? VL : 1) * elem_bytes));
+        const i64 p = passes(sl, (int)((block ? VS : contig ? VL : 1) * elem_bytes), false);
         *wr += p - (lanes + 63) / 64 * std::max<i64>(1, (block ? VS : contig ? VL : 1) * elem_bytes * 64 / 128);
       }
     }
     for (i64 q0 = 0; q0 < TILE / VS; q0 += 64) {
       sl.clear();
       for (i64 l = 0; l < std::min<i64>(64, TILE / VS - q0); ++l) sl.push_back(slot_num((q0 + l) * VS, S, S2));
-      *rd += passes(sl, (int)(VS * elem_bytes)) - std::max<i64>(1, VS * elem_bytes * 64 / 128);
+      *rd += passes(sl, (int)(VS * elem_bytes), true) - std::max<i64>(1, VS * elem_bytes * 64 / 256);
     }
   };
   // Candidates: rows of 256 and of 128 bytes (the latter keep two vectors
