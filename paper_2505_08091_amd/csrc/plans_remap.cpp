@@ -273,21 +273,34 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
   // ends mid-line at a box edge and the rest of the line belongs to the
   // neighbouring box (above, below, left or right) along that antidiagonal:
   // the two write or fetch the shared line once each unless it meets both in
-  // one L2.  Workgroups are dispatched round-robin over the 8 XCDs, and XCD x
-  // takes the x-th eighth of the order; with the grid in 2 x 2 tiles of
-  // (n/2) x (n/2) boxes, row-major inside, each eighth is a compact
-  // (n/4) x (n/2) rectangle of boxes walked row by row, so most neighbours
-  // share an XCD and run close in time.  Measured against the antidiagonal
-  // order of the boxes (8192^2 fp32, 128 x 128 boxes: 5.32 / 6.02 ->
-  // 5.44 / 6.66 TB/s; 4096^2: 5.33 / 5.99 -> 5.72 / 5.95; fp16 4096^2: 4.35 /
-  // 4.71 -> 4.38 / 4.93), Morton order and tiles of 8 or 16 boxes.
+  // one L2 while it is still there.  Workgroups are dispatched round-robin
+  // over the 8 XCDs, and XCD x takes the x-th eighth of the order; with the
+  // grid in 2 x 2 tiles of (n/2) x (n/2) boxes, each eighth is a compact
+  // (n/4) x (n/2) rectangle of boxes, walked row by row.  When an XCD holds
+  // too few boxes at once for a box and the one below it to run together
+  // (fewer than 8 rows of the rectangle: 128 x 128 fp32 boxes, two per CU),
+  // a destination in antidiagonal order walks the rectangle in bands of 4
+  // rows, column by column, so that neighbours run close in time and the
+  // partial lines merge in the L2 (8192^2 fp32 forward: writes +13.5% ->
+  // +4.4% over the algorithmic bytes, 5.40-5.45 -> 5.52-5.54 TB/s; reading
+  // antidiagonals, the row-by-row walk measured faster).  Measured against
+  // the antidiagonal order of the boxes (8192^2 fp32: 5.32 / 6.02 -> 5.52 /
+  // 6.66 TB/s; 4096^2: 5.33 / 5.99 -> 5.72 / 5.95), Morton order and tiles
+  // of 8 or 16 boxes.
   const bool ad_lines = os == 2 || od == 2;
   const bool xcd = nb % 8 == 0;
   long long bt = ad_lines && nbr == nbc && nbr % 2 == 0 && xcd ? nbr / 2 : 0;
   bt = tune("remap.box_tile", bt);
   const bool ad_boxes = bt > 0 && nbr % bt == 0 && nbc % bt == 0;
-  const LayoutP Wb = ad_boxes ? make_tileorderby({make_row({nbr / bt, nbc / bt}), make_row({bt, bt})})
-                              : make_from_piece(make_row({nbr, nbc}));
+  const i64 per_cu = std::max<i64>(1, std::min<i64>(8, (160 * 1024) / (B * B * elem_bytes)));
+  long long band = od == 2 && 32 * per_cu < 8 * bt ? 4 : 0;
+  band = tune("remap.box_band", band);
+  LayoutP Wb = ad_boxes ? make_tileorderby({make_row({nbr / bt, nbc / bt}), make_row({bt, bt})})
+                        : make_from_piece(make_row({nbr, nbc}));
+  if (ad_boxes && band > 0 && bt % band == 0)
+    Wb = make_tileorderby({make_row({nbr / bt, nbc / bt}), make_row({bt / band, 1}), make_col({band, bt})});
+  else
+    band = 0;
   auto box_fn = [&](Ctx& c) {
     int b = c.var("b", nb);
     SymAlg al{&c};
@@ -398,7 +411,8 @@ static bool plan_remap_box(const Layout& src, const Layout& dst, int elem_bytes,
   R.block = NT;
   R.grid = nb;
   R.src = s.str();
-  R.info = "box " + std::to_string(B) + "x" + std::to_string(B) + (ad_boxes ? " tiles" + std::to_string(bt) : " row") +
+  R.info = "box " + std::to_string(B) + "x" + std::to_string(B) +
+           (ad_boxes ? " tiles" + std::to_string(bt) + (band ? "-bands" + std::to_string(band) : "") : " row") +
            (xcd ? "-xcd" : "") + " load " + names[os] + (ssep ? " sep" : " full") + " (" + std::to_string(bs) +
            " runs) store " + names[od] + (dsep ? " sep" : " full") + " (" + std::to_string(bd) + " runs) pad " +
            std::to_string(pad) + (nontemporal & 1 ? " nt-loads" : "") + (nontemporal & 2 ? " nt-stores" : "") +

@@ -5,7 +5,7 @@
 // gemm.direct, gemm.prefetch, gemm.rolling, gemm.dma_spread, gemm.frag_dist,
 // gemm.frag_spread, gemm.store_at, gemm.persist, gemm.ring_unroll, gemm.wide_waves,
 // gemm.dma_rows, index.nt_store, index.grid, remap.nontemporal, remap.box,
-// remap.box_side, remap.box_tile, remap.nt, remap.unroll, remap.order (0 destination, 1
+// remap.box_side, remap.box_tile, remap.box_band, remap.nt, remap.unroll, remap.order (0 destination, 1
 // source), remap.xcd, remap.persist, remap.tile_bytes, remap.block (LDS block
 // transfer), remap.swizzle, remap.swizzle2, remap.lds_row (LDS XOR key strides
 // and row bytes).

@@ -72,6 +72,29 @@ def test_remap_transpose(lego, n, dtype):
         assert (bits(out) == exp).all(), name
 
 
+@pytest.mark.parametrize("n,dtype", [(4096, "f32"), (8192, "f32"), (4096, "f16")])
+def test_remap_antidiagonal_full(lego, n, dtype):
+    """Row -> antidiagonal order (Figure 7's GenP over the whole matrix) and
+    back, each direction on its own source, every element against the
+    oracle's remap: the box plans the bench measures (128 x 128 boxes beyond
+    the last-level cache, the forward walking its rectangle of boxes in
+    bands)."""
+    dev = need_gpu()
+    row, ad = lego.as_layout(lego.Row(n, n)), lego.as_layout(lego.GenP("antidiag", [n, n]))
+    orow, oad = OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.antidiag_genp(n))
+    for seed, (ls, ld, ols, old, name) in enumerate(((row, ad, orow, oad, "row->antidiag"),
+                                                     (ad, row, oad, orow, "antidiag->row"))):
+        src = S.tensor(n * n, dtype, seed=S.SEED_SRC + seed)
+        info = lego.remap_plan(ls, ld, src.element_size())["info"]
+        say(f"remap antidiagonal {name} n={n} {dtype} plan={info}")
+        assert info.startswith("box "), info
+        if n == 8192 and seed == 0:
+            assert info.startswith("box 128x128 tiles32-bands4-xcd "), info
+        out = _run(lego, ls, ld, src, dev)
+        exp = OR.remap(ols, old, bits(src))
+        assert (bits(out) == exp).all(), name
+
+
 @pytest.mark.parametrize("b", [8, 4])
 def test_remap_bricks_512cubed_sampled(lego, b):
     """512^3 fp32 Row <-> bricks of b^3 (the configuration the bench times):
