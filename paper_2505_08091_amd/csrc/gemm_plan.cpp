@@ -104,6 +104,17 @@ LayoutP tr_lds(i64 rows, i64 k) {
   return base;
 }
 
+// LDS tile for an operand stored in Z order (Morton), whose 16-byte global
+// vectors are 2 x 4 blocks of the tile with element bits (k, m, k): each block
+// keeps one 16-byte LDS slot in its global order, so it is copied unchanged,
+// and the slots of block row r are XOR-permuted by r (a GenP over
+// [rows/2, k/4]): the 16 blocks of rows 0-31 at one k, which one half of a
+// wave's fragment read touches, fall in 16 distinct granules of a 256-byte
+// bank window.  As a layout: TileOrderBy(XOR[rows/2, k/4], Col[2, 2], Row[1, 2]).
+LayoutP z_lds(i64 rows, i64 k) {
+  return make_tileorderby({make_genp(GEN_XOR_SWIZZLE, {rows / 2, k / 4}, {1, 1}), make_col({2, 2}), make_row({1, 2})});
+}
+
 void need_dims(const LayoutP& l, std::vector<i64> d, const char* what) {
   if (l->dims() != d) throw std::length_error(std::string(what) + " layout has the wrong logical shape");
   if (l->expand_inner) throw Unsupported(std::string(what) + ": ExpandBy layouts are not supported by the GEMM");
@@ -137,6 +148,8 @@ struct Operand {
   i64 NVEC = 0;
   bool guard = false, sep = false, svec = false, frvec = false;
   bool frtr = false;      // fragments read with the transposing LDS load
+  bool frdw = false;      // fragments read as 4 dwords of 2 consecutive k each
+  i64 frdw_d = 0;         // element distance of dwords 2h and 2h + 1 (0: not constant)
   i64 rows_total = 0;     // M (A) or N (B): logical extent along the tile rows
   bool edge = false;      // some loads fall outside the operand (padded tiles)
   bool user_lds = false;  // LDS layout given by the caller
@@ -234,6 +247,76 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   need_dims(SB, {bn, bk}, "LDS B");
   LayoutP FA = mfma_fragment_layout(MB == 32 ? 0 : 1, 0);
   LayoutP FC = mfma_fragment_layout(MB == 32 ? 0 : 1, 2);
+
+  // How a wave reads its MFMA fragments of operand `o` from its LDS layout:
+  // one 16-byte vector per lane, the transposing load, 4 dwords of two
+  // consecutive k each, or element by element.
+  auto frag_modes = [&](Operand& o) {
+    o.frvec = o.frtr = o.frdw = false;
+    // Vector fragment read?
+    {
+      Ctx c;
+      int lane = c.var("lane", 64), w = c.var("w", NWAVES), mi = c.var("mi", o.is_b ? NI : MI),
+          s = c.var("s", bk / KB), e = c.var("e", 8);
+      SymAlg al{&c};
+      Sum f = FA->apply(al, {var(c, lane), var(c, e)});
+      Sum r = fdiv(c, f, KB), k = fmod(c, f, KB);
+      Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+      Sum kk = add(c, mulc(c, var(c, s), KB), k);
+      o.frvec = contiguous_in(o.lds->apply(al, {row, kk}), e, 8);
+    }
+    // Transposing fragment read (ds_read_b64_tr_b16): in each 16-lane block b,
+    // lane i receives element j from the address of lane 16b + 4j + i/4 plus
+    // i%4.  It serves a fragment when 4 lanes 4q..4q+3 of a block hold 4
+    // consecutive rows at equal k (checked on the fragment layout) and 4
+    // consecutive rows are 4 contiguous LDS elements, 4-aligned (checked on
+    // the LDS layout).
+    if (!o.frvec) {
+      IntAlg ia;
+      bool lanes_ok = true;
+      for (i64 l0 = 0; l0 < 64 && lanes_ok; l0 += 4)
+        for (i64 e = 0; e < 8 && lanes_ok; ++e) {
+          i64 f0 = FA->apply(ia, {l0, e});
+          for (i64 t = 1; t < 4; ++t)
+            if (FA->apply(ia, {l0 + t, e}) != f0 + t * KB) lanes_ok = false;
+        }
+      Ctx c;
+      int w = c.var("w", NWAVES), mi = c.var("mi", o.is_b ? NI : MI), rr = c.var("rr", MB / 4),
+          kq = c.var("kq", bk), t = c.var("t", 4);
+      SymAlg al{&c};
+      Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)),
+                    add(c, mulc(c, var(c, rr), 4), var(c, t)));
+      o.frtr = lanes_ok && contiguous_in(o.lds->apply(al, {row, var(c, kq)}), t, 4);
+    }
+    // Dword reads: fragment elements 2p and 2p + 1 adjacent in LDS, the pair
+    // 4-byte aligned (p = 2h + t).  When the offset moves by a constant D
+    // from t = 0 to t = 1, each half h is one address and the read pairs
+    // (that address, + D) become single ds_read2_b32 instructions.
+    if (!o.frvec && !o.frtr) {
+      Ctx c;
+      int lane = c.var("lane", 64), w = c.var("w", NWAVES), mi = c.var("mi", o.is_b ? NI : MI),
+          s = c.var("s", bk / KB), h = c.var("h", 2), t = c.var("t", 2), q = c.var("q", 2);
+      SymAlg al{&c};
+      Sum e = add(c, add(c, mulc(c, var(c, h), 4), mulc(c, var(c, t), 2)), var(c, q));
+      Sum f = FA->apply(al, {var(c, lane), e});
+      Sum r = fdiv(c, f, KB), k = fmod(c, f, KB);
+      Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+      Sum kk = add(c, mulc(c, var(c, s), KB), k);
+      const Sum off = o.lds->apply(al, {row, kk});
+      o.frdw = contiguous_in(off, q, 2);
+      o.frdw_d = 0;
+      Sum pt, rest;
+      std::vector<int> g = {t};
+      if (o.frdw && split_by(off, g, &pt, &rest) && pt.c0 == 0 && pt.t.size() == 1) {
+        const Atom& a = *pt.t[0].a;
+        if (a.op == Op::Field && a.var == t && a.a == 1 && a.b == 0 && pt.t[0].c > 0 && pt.t[0].c % 2 == 0)
+          o.frdw_d = pt.t[0].c;
+      }
+    }
+  };
 
   Operand ops[2] = {{bm, bk, LA, SA, false}, {bn, bk, LB, SB, true}};
   ops[0].user_lds = (bool)rq.lds_a;
@@ -405,51 +488,30 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
         if (o.V == 1) o.svec = true;
       }
     }
-    // Vector fragment read?
-    {
-      Ctx c;
-      int lane = c.var("lane", 64), w = c.var("w", NWAVES), mi = c.var("mi", o.is_b ? NI : MI),
-          s = c.var("s", bk / KB), e = c.var("e", 8);
-      SymAlg al{&c};
-      Sum f = FA->apply(al, {var(c, lane), var(c, e)});
-      Sum r = fdiv(c, f, KB), k = fmod(c, f, KB);
-      Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
-      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
-      Sum kk = add(c, mulc(c, var(c, s), KB), k);
-      o.frvec = contiguous_in(o.lds->apply(al, {row, kk}), e, 8);
-    }
-    // Transposing fragment read (ds_read_b64_tr_b16): in each 16-lane block b,
-    // lane i receives element j from the address of lane 16b + 4j + i/4 plus
-    // i%4.  It serves a fragment when 4 lanes 4q..4q+3 of a block hold 4
-    // consecutive rows at equal k (checked on the fragment layout) and 4
-    // consecutive rows are 4 contiguous LDS elements, 4-aligned (checked on
-    // the LDS layout).
-    if (!o.frvec) {
-      IntAlg ia;
-      bool lanes_ok = true;
-      for (i64 l0 = 0; l0 < 64 && lanes_ok; l0 += 4)
-        for (i64 e = 0; e < 8 && lanes_ok; ++e) {
-          i64 f0 = FA->apply(ia, {l0, e});
-          for (i64 t = 1; t < 4; ++t)
-            if (FA->apply(ia, {l0 + t, e}) != f0 + t * KB) lanes_ok = false;
-        }
-      Ctx c;
-      int w = c.var("w", NWAVES), mi = c.var("mi", o.is_b ? NI : MI), rr = c.var("rr", MB / 4),
-          kq = c.var("kq", bk), t = c.var("t", 4);
-      SymAlg al{&c};
-      Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
-      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)),
-                    add(c, mulc(c, var(c, rr), 4), var(c, t)));
-      o.frtr = lanes_ok && contiguous_in(o.lds->apply(al, {row, var(c, kq)}), t, 4);
-    }
+    frag_modes(o);
   }
 
+  // Z-order operands (2 x 4 blocks with element bits k, m, k) can be copied
+  // directly into the z_lds layout, which keeps each block in one LDS slot;
+  // a lane then reads its row's 8 k as 4 dwords (2 k each).
+  LayoutP zl[2];
+  for (int k = 0; k < 2; ++k) {
+    const Operand& o = ops[k];
+    if (o.user_lds || o.axis != 2 || o.VR != 2 || o.VC != 4 || o.bdi != std::vector<i64>{0, 1, 0} ||
+        o.bdj != std::vector<i64>{1, 0, 2} || o.R % 2 || o.KD % 8 || !pow2(o.KD / 4) || !tune("gemm.zdirect", 1))
+      continue;
+    Operand t = o;
+    t.lds = z_lds(o.R, o.KD);
+    frag_modes(t);
+    if (t.frdw) zl[k] = t.lds;
+  }
   // Direct global-to-LDS copies need 16-byte global runs under the inverse
   // LDS layout and whole rounds of load vectors.
   bool direct = true;
   direct = tune("gemm.direct", 1) != 0;
   if ((bk / KB) % 2) direct = false;  // the direct loop alternates fragment buffers per substep
-  for (Operand& o : ops) {
+  for (int k = 0; k < 2; ++k) {
+    const Operand& o = ops[k];
     if (!direct) break;
     if ((o.R * o.KD) % (8 * NT)) {
       direct = false;
@@ -457,6 +519,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
     }
     Operand t = o;
     t.direct = true;
+    if (zl[k]) t.lds = zl[k];
     t.V = 8;
     t.NV = (int)(o.R * o.KD / 8 / NT);
     Ctx c;
@@ -472,7 +535,12 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
       direct = false;
   }
   if (direct) {
-    for (Operand& o : ops) {
+    for (int k = 0; k < 2; ++k) {
+      Operand& o = ops[k];
+      if (zl[k]) {
+        o.lds = zl[k];
+        frag_modes(o);
+      }
       o.direct = true;
       o.V = 8;
       o.axis = 1;
@@ -633,6 +701,24 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
                        f.outs = {in_range(c, oo, var(c, tt), var(c, kt), i, j)};
                        return f;
                      }});
+    if (o.frdw && o.frdw_d)
+      fns.push_back({p + "fd", [&, k](Ctx& c) {
+                       // LDS offset of fragment element 4h: the first dword of
+                       // half h (the second lies FRDW_D elements further).
+                       const Operand& oo = ops[k];
+                       int lane = c.var("lane", 64), w = c.var("w", NWAVES), mi = c.var("mi", oo.is_b ? NI : MI),
+                           s = c.var("s", bk / KB), h = c.var("h", 2);
+                       SymAlg al{&c};
+                       Sum f0 = FA->apply(al, {var(c, lane), mulc(c, var(c, h), 4)});
+                       Sum r = fdiv(c, f0, KB), kq = fmod(c, f0, KB);
+                       Sum wpos = oo.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
+                       Sum row = add(c, add(c, mulc(c, wpos, oo.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+                       Sum kk = add(c, mulc(c, var(c, s), KB), kq);
+                       FnSpec f;
+                       f.params = {lane, w, mi, s, h};
+                       f.outs = {oo.lds->apply(al, {row, kk})};
+                       return f;
+                     }});
     if (o.frtr)
       fns.push_back({p + "ft", [&, k](Ctx& c) {
                        // Address lane `lane` supplies to the transposing read of
@@ -749,6 +835,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
     s << "#define " << P2[k] << "NV " << o.NV << "\n#define " << P2[k] << "V " << o.V << "\n#define " << P2[k]
       << "SEP " << (o.sep ? 1 : 0) << "\n#define " << P2[k] << "SVEC " << (o.svec ? 1 : 0) << "\n#define " << P2[k]
       << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "FRTR " << (o.frtr ? 1 : 0) << "\n#define " << P2[k]
+      << "FRDW " << (o.frdw ? 1 : 0) << "\n#define " << P2[k] << "FRDW_D " << o.frdw_d << "\n#define " << P2[k]
       << "NVEC " << o.NVEC << "u\n#define " << P2[k]
       << "GUARD " << (o.guard ? 1 : 0) << "\n#define " << P2[k] << "EDGE " << (o.edge ? 1 : 0) << "\n#define "
       << P2[k] << "BUF " << (o.direct && 2 * o.glob->phys_size() < (i64(1) << 31) ? 1 : 0) << "\n#define "
@@ -791,7 +878,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // that reads held up by copies landing in LDS do not stall them (0.857 ->
   // 0.852 ms on the 8192^3 bf16 GEMM); not with the transposing reads, whose
   // wait at each substep covers every read in flight.
-  int frag_dist = (ops[0].frtr || ops[1].frtr) ? 1 : 2;
+  int frag_dist = 2;
   frag_dist = (int)std::max<long long>(1, std::min<long long>(3, tune("gemm.frag_dist", frag_dist)));
   // (Reads two substeps ahead need three substeps per step: with two, the
   // early reads of the last substep would replace fragments its later MFMA
@@ -830,10 +917,10 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
        << MB << "x" << KB << " sched" << (xcd ? "+xcd" : "") << " A:V" << ops[0].V
        << (ops[0].gaxis == 2 ? "b" + std::to_string(ops[0].VR) + "x" + std::to_string(ops[0].VC) : (ops[0].gaxis ? "k" : "m"))
        << (ops[0].sep ? " sep" : " full") << (ops[0].svec ? " svec" : " sscalar")
-       << (ops[0].frvec ? " frvec" : (ops[0].frtr ? " frtr" : " frscalar")) << " B:V" << ops[1].V
+       << (ops[0].frvec ? " frvec" : (ops[0].frtr ? " frtr" : (ops[0].frdw ? " frdw" : " frscalar"))) << " B:V" << ops[1].V
        << (ops[1].gaxis == 2 ? "b" + std::to_string(ops[1].VR) + "x" + std::to_string(ops[1].VC) : (ops[1].gaxis ? "k" : "n"))
        << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
-       << (ops[1].frvec ? " frvec" : (ops[1].frtr ? " frtr" : " frscalar")) << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
+       << (ops[1].frvec ? " frvec" : (ops[1].frtr ? " frtr" : (ops[1].frdw ? " frdw" : " frscalar"))) << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")
        << (direct ? " direct-lds" : " staged")
        << (direct ? std::string(dma_spread ? " spread" : " burst") + " fd" + std::to_string(frag_dist) : "")
        << (ragged_groups ? " ragged-groups" : "")

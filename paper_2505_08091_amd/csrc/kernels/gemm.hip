@@ -27,6 +27,10 @@
 //   a_fr(lane, w, mi, s, e)          LDS element offset of fragment element e
 //   A_FRTR, a_ft(lane, w, mi, s, h)  fragments read with the transposing LDS
 //                                    load: the address lane supplies for half h
+//   A_FRDW                           fragments read as 4 dwords at a_fr(.., 2p),
+//                                    elements 2p and 2p + 1 adjacent in LDS;
+//   A_FRDW_D, a_fd(lane, w, mi, s, h)  with A_FRDW_D > 0, dword 2h at a_fd(h)
+//                                    and dword 2h + 1 A_FRDW_D elements on
 //   (b_* likewise with tn)
 //   c_t(tm, tn) c_l(lane, w, mi, ni, r)   or   c_f(tm, tn, lane, w, mi, ni, r)
 //   A_BUF (and B_BUF): direct copies are range-checked buffer loads with
@@ -74,6 +78,15 @@ typedef float acc_t __attribute__((ext_vector_type(4)));
 LEGO_FN mf_t lds_frag(const elem_t* base, IDX_T off) {
   return __builtin_bit_cast(mf_t, *(const e8_t*)(base + off));
 }
+// Fragment as 4 dwords, each 2 consecutive k of the lane's row (Z-order
+// operands, whose LDS slots interleave two rows); reads whose offsets differ
+// by a constant pair up into ds_read2_b32.
+LEGO_FN mf_t lds_frag_dw(const elem_t* base, IDX_T o0, IDX_T o1, IDX_T o2, IDX_T o3) {
+  typedef unsigned u4_t __attribute__((ext_vector_type(4)));
+  const u4_t t = {*(const unsigned*)(base + o0), *(const unsigned*)(base + o1), *(const unsigned*)(base + o2),
+                  *(const unsigned*)(base + o3)};
+  return __builtin_bit_cast(mf_t, t);
+}
 
 // Fragment through two transposing LDS loads (ds_read_b64_tr_b16): elements
 // 0-3 from the addresses of half 0, elements 4-7 from those of half 1.  The
@@ -104,10 +117,23 @@ LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
     __builtin_amdgcn_s_waitcnt(0xC07F);     \
     __builtin_amdgcn_sched_barrier(0);      \
   } while (0)
+// Start of a substep of the direct-copy loop: the fragments of this substep
+// must have arrived, those of the FRAG_DIST - 1 substeps after it may still
+// be in flight.  A wave's LDS operations complete in issue order, and at
+// least FRAG_READS of them were issued per substep after this substep's last
+// read, so waiting until at most (FRAG_DIST - 1) * FRAG_READS (the counter
+// holds 15) are outstanding is enough.
+#define LGKM_NEXT ((FRAG_DIST - 1) * FRAG_READS < 15 ? (FRAG_DIST - 1) * FRAG_READS : 15)
+#define FRAG_WAIT_NEXT()                                  \
+  do {                                                    \
+    __builtin_amdgcn_s_waitcnt(0xC07F | (LGKM_NEXT << 8)); \
+    __builtin_amdgcn_sched_barrier(0);                    \
+  } while (0)
 #else
 #define FRAG_WAIT() \
   do {              \
   } while (0)
+#define FRAG_WAIT_NEXT() FRAG_WAIT()
 #endif
 // Fragment register sets: FRAG_DIST + 1, or one per substep when that does
 // not divide the substeps of a step (a set's index must repeat every step).
@@ -132,8 +158,8 @@ LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
 // FRAG_DIST.
 static_assert(FRAG_DIST == 1 || (FRAG_DIST < BK / KB && NFB > FRAG_DIST), "fragment sets");
 // LDS read instructions per fragment.
-#define A_FRD (A_FRTR ? 2 : (A_FRVEC ? 1 : 8))
-#define B_FRD (B_FRTR ? 2 : (B_FRVEC ? 1 : 8))
+#define A_FRD (A_FRTR ? 2 : (A_FRVEC ? 1 : (A_FRDW ? 2 : 8)))
+#define B_FRD (B_FRTR ? 2 : (B_FRVEC ? 1 : (B_FRDW ? 2 : 8)))
 #define FRAG_READS (MI * A_FRD + NI * B_FRD)
 
 template <bool B>
@@ -304,6 +330,14 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       af[buf][i] = lds_frag_tr(la, a_ft(lane, w, i, s, 0), a_ft(lane, w, i, s, 1));
 #elif A_FRVEC
       af[buf][i] = lds_frag(la, a_fr(lane, w, i, s, 0));
+#elif A_FRDW && A_FRDW_D
+      {
+        const IDX_T o0 = a_fd(lane, w, i, s, 0), o1 = a_fd(lane, w, i, s, 1);
+        af[buf][i] = lds_frag_dw(la, o0, o0 + A_FRDW_D, o1, o1 + A_FRDW_D);
+      }
+#elif A_FRDW
+      af[buf][i] = lds_frag_dw(la, a_fr(lane, w, i, s, 0), a_fr(lane, w, i, s, 2), a_fr(lane, w, i, s, 4),
+                               a_fr(lane, w, i, s, 6));
 #else
       e8_t t;
 #pragma unroll
@@ -318,6 +352,14 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       bf[buf][j] = lds_frag_tr(lb, b_ft(lane, w, j, s, 0), b_ft(lane, w, j, s, 1));
 #elif B_FRVEC
       bf[buf][j] = lds_frag(lb, b_fr(lane, w, j, s, 0));
+#elif B_FRDW && B_FRDW_D
+      {
+        const IDX_T o0 = b_fd(lane, w, j, s, 0), o1 = b_fd(lane, w, j, s, 1);
+        bf[buf][j] = lds_frag_dw(lb, o0, o0 + B_FRDW_D, o1, o1 + B_FRDW_D);
+      }
+#elif B_FRDW
+      bf[buf][j] = lds_frag_dw(lb, b_fr(lane, w, j, s, 0), b_fr(lane, w, j, s, 2), b_fr(lane, w, j, s, 4),
+                               b_fr(lane, w, j, s, 6));
 #else
       e8_t t;
 #pragma unroll
@@ -512,7 +554,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     const elem_t* na = lds + ((cur_stage + 1) % NSTAGES) * STAGE;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
-      FRAG_WAIT();
+      FRAG_WAIT_NEXT();
       if (s == S - FRAG_DIST) {
         // Every read of stage `cur_stage` has been issued and has completed
         // (the barrier waits for this wave's LDS reads).  Once the next step's

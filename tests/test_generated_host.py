@@ -384,6 +384,31 @@ int main() {
 #endif
     }
 #endif
+  // dword fragment reads: elements 2p, 2p + 1 adjacent and 4-byte aligned;
+  // with a constant distance D, dword 2h at a_fd(h) and dword 2h + 1 at +D
+#if A_FRDW || B_FRDW
+  for (u64 w = 0; w < NWAVES; ++w)
+    for (u64 s = 0; s < BK / KB; ++s) for (u64 l = 0; l < 64; ++l) for (u64 p = 0; p < 4; ++p) {
+#if A_FRDW
+      for (u64 mi = 0; mi < MI; ++mi) {
+        u64 o = a_fr((IDX_T)l, (IDX_T)w, (IDX_T)mi, (IDX_T)s, (IDX_T)(2 * p));
+        if (o % 2 || (u64)a_fr((IDX_T)l, (IDX_T)w, (IDX_T)mi, (IDX_T)s, (IDX_T)(2 * p + 1)) != o + 1) FAIL("a_fr dword pair");
+#if A_FRDW_D
+        if ((u64)a_fd((IDX_T)l, (IDX_T)w, (IDX_T)mi, (IDX_T)s, (IDX_T)(p / 2)) + (p % 2) * A_FRDW_D != o) FAIL("a_fd mismatch");
+#endif
+      }
+#endif
+#if B_FRDW
+      for (u64 ni = 0; ni < NI; ++ni) {
+        u64 o = b_fr((IDX_T)l, (IDX_T)w, (IDX_T)ni, (IDX_T)s, (IDX_T)(2 * p));
+        if (o % 2 || (u64)b_fr((IDX_T)l, (IDX_T)w, (IDX_T)ni, (IDX_T)s, (IDX_T)(2 * p + 1)) != o + 1) FAIL("b_fr dword pair");
+#if B_FRDW_D
+        if ((u64)b_fd((IDX_T)l, (IDX_T)w, (IDX_T)ni, (IDX_T)s, (IDX_T)(p / 2)) + (p % 2) * B_FRDW_D != o) FAIL("b_fd mismatch");
+#endif
+      }
+#endif
+    }
+#endif
   // epilogue: every C element written exactly once
   {
     std::vector<char> c(GEMM_M * GEMM_N);
@@ -588,10 +613,12 @@ def _gemm_cases():
     cases.append(dict(M=1024, N=1024, K=1024, dtype="bf16", lds_a=sw, lds_b=sw))
     from tests.test_gpu_gemm import _persistent_cases
     cases += [{k: v for k, v in c.items() if k not in ("oa", "ob", "max_workgroups")} for c in _persistent_cases(L)]
+    from tests.test_gpu_gemm import _morton_direct_cases, _morton_direct_kw
+    cases += [{k: v for k, v in _morton_direct_kw(L, c).items() if k != "max_workgroups"} for c in _morton_direct_cases(L)]
     return cases
 
 
-N_GEMM_CASES = 41
+N_GEMM_CASES = 45
 
 
 def test_gemm_case_count():

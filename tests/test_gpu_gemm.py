@@ -224,6 +224,50 @@ def test_gemm_c5_morton_a(lego):
     assert ok, (mre, fre)
 
 
+def _morton_direct_cases(L):
+    """Morton-order A copied directly into LDS (each 2 x 4 Z block in one
+    slot) and read as dword pairs: bf16 with column-major B, smaller tiles
+    with row-major B (the transposing read beside it), 32-deep k-steps, and a
+    workgroup walking several tiles."""
+    return [
+        dict(M=1024, N=1024, K=1024, dtype="bf16", bl="Col"),
+        dict(M=1024, N=512, K=2048, dtype="f16", bl="Row", bm=128, bn=128, bk=64, wm=64, wn=64),
+        dict(M=512, N=512, K=512, dtype="f16", bl="Col", bm=128, bn=128, bk=32, wm=64, wn=64),
+        dict(M=1024, N=1024, K=512, dtype="f16", bl="Row", max_workgroups=5),
+    ]
+
+
+def _morton_direct_kw(L, case):
+    kw = {k: v for k, v in case.items() if k not in ("bl",)}
+    kw["a"] = L.as_layout(L.GenP("morton", [case["M"], case["K"]]))
+    kw["b"] = L.as_layout(getattr(L, case["bl"])(case["K"], case["N"]))
+    return kw
+
+
+@pytest.mark.parametrize("i", range(4))
+def test_gemm_morton_a_direct(lego, i):
+    """Morton-A GEMMs on the direct-copy path with dword fragment reads,
+    every output element against the fp64 oracle reading A through its
+    Morton layout (the A buffer made by the oracle's remap)."""
+    import torch
+    case = _morton_direct_cases(lego)[i]
+    kw = _morton_direct_kw(lego, case)
+    M, N, K, dt = kw.pop("M"), kw.pop("N"), kw.pop("K"), kw.pop("dtype")
+    a_log = S.tensor(M * K, dt, seed=S.SEED_A)
+    b = S.tensor(K * N, dt, seed=S.SEED_B)
+    omz = OL.as_layout(OL.morton_genp(M, K))
+    a_mz_bits = OR.remap(OL.as_layout(OL.Row(M, K)), omz, S.as_numpy_bits(a_log))
+    a_mz = torch.from_numpy(a_mz_bits.view(np.int16).copy()).view(a_log.dtype)
+    plan = lego.gemm_plan(M, N, K, dt, **{k: v for k, v in kw.items() if k != "max_workgroups"})
+    say(f"gemm Morton-A direct {case} plan={plan}")
+    assert "frdw" in plan and "direct-lds" in plan, plan
+    c = _run(lego, a_mz, b, M, N, K, dt, **kw).reshape(M, N)
+    assert np.isfinite(c).all()
+    r = OG.gemm(a_mz_bits, S.as_numpy_bits(b), omz, OL.as_layout(getattr(OL, case["bl"])(K, N)), dt)
+    ok, mre, fre = OG.check_tolerance(c, r)
+    assert ok, (mre, fre)
+
+
 @pytest.mark.parametrize("la_name,lb_name", [("Row", "Row"), ("Row", "Col"), ("Col", "Row"), ("Col", "Col")])
 def test_gemm_operand_layouts_4096(lego, la_name, lb_name):
     """The four Row/Col operand variants of Section V-A at 4096^3 fp16 with

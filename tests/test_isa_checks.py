@@ -62,24 +62,31 @@ def vregs(ops):
     return regs
 
 
+_LGKM = re.compile(r"lgkmcnt\((\d+)\)")
+
+
 def untracked_load_violations(insts, load="ds_read_b64_tr_b16"):
-    """For every `load`, the instructions reachable from it before an
-    s_waitcnt lgkmcnt(0) that read or write one of its destination
-    registers."""
+    """For every `load`, the instructions reachable from it before a wait
+    that covers it and that read or write one of its destination registers.
+    A wave's LDS operations complete in issue order, so s_waitcnt
+    lgkmcnt(N) covers the load once at least N LDS operations (ds_*) were
+    issued after it on the path; other counted operations (scalar loads)
+    complete out of order and are not counted."""
     index = {a: i for i, (a, _, _, _) in enumerate(insts)}
     bad = []
     for i, (addr, mnem, ops, _) in enumerate(insts):
         if mnem != load:
             continue
         dest = vregs(ops.split(",")[0])
-        seen, stack = set(), [i + 1]
+        seen, stack = set(), [(i + 1, 0)]
         while stack:
-            j = stack.pop()
-            if j in seen or j >= len(insts):
+            j, later = stack.pop()
+            if (j, later) in seen or j >= len(insts):
                 continue
-            seen.add(j)
+            seen.add((j, later))
             a, m, o, tgt = insts[j]
-            if m == "s_waitcnt" and "lgkmcnt(0)" in o:
+            w = _LGKM.search(o) if m == "s_waitcnt" else None
+            if w and later >= int(w.group(1)):
                 continue
             if m == load and vregs(o.split(",")[0]) == dest and not (vregs(o.split(",", 1)[1]) & dest):
                 # another load into the same registers: the LDS returns one
@@ -91,10 +98,11 @@ def untracked_load_violations(insts, load="ds_read_b64_tr_b16"):
                 continue
             if m == "s_endpgm":
                 continue
+            nl = min(later + 1, 16) if m.startswith("ds_") else later
             if tgt is not None:
-                stack.append(index[tgt])
+                stack.append((index[tgt], nl))
             if m != "s_branch":
-                stack.append(j + 1)
+                stack.append((j + 1, nl))
     return bad
 
 
@@ -136,6 +144,23 @@ def test_checker_finds_a_planted_early_use():
     assert len(untracked_load_violations(parse(loop))) == 1
     ok = loop.replace("\tv_mov_b32_e32 v20, v11  // 000000001000: 0", "\ts_nop 0  // 000000001000: 0")
     assert untracked_load_violations(parse(ok)) == []
+
+
+def test_checker_counts_later_lds_operations():
+    """s_waitcnt lgkmcnt(N) covers a load only when N LDS operations were
+    issued after it; a scalar load in between does not count."""
+    def prog(between, n):
+        lines = ["0000000000001000 <k>:", "\tds_read_b64_tr_b16 v[10:11], v3  // 000000001000: 0"]
+        for i, b in enumerate(between):
+            lines.append(f"\t{b}  // {0x1008 + 8 * i:012X}: 0")
+        lines += [f"\ts_waitcnt lgkmcnt({n})  // 000000001100: 0", "\tv_mov_b32_e32 v20, v11  // 000000001104: 0",
+                  "\ts_endpgm  // 000000001108: 0"]
+        return parse("\n".join(lines))
+    two = ["ds_read_b128 v[20:23], v4", "ds_read2_b32 v[24:25], v5 offset1:2"]
+    assert untracked_load_violations(prog(two, 2)) == []
+    assert untracked_load_violations(prog(two, 1)) == []
+    assert len(untracked_load_violations(prog(two, 3))) == 1
+    assert len(untracked_load_violations(prog(two[:1] + ["s_load_dword s4, s[0:1], 0x0"], 2))) == 1
 
 
 def test_generated_kernels_do_not_spill(dumped):
