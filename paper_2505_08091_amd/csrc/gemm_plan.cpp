@@ -150,6 +150,8 @@ struct Operand {
   bool frtr = false;      // fragments read with the transposing LDS load
   bool frdw = false;      // fragments read as 4 dwords of 2 consecutive k each
   i64 frdw_d = 0;         // element distance of dwords 2h and 2h + 1 (0: not constant)
+  bool mpair = false;     // MFMA blocks 2m, 2m+1 take the even / odd rows of a 2*MB band (A only)
+  bool frzp = false;      // with mpair: both fragments from two 16-byte reads of 2 x 4 blocks
   i64 rows_total = 0;     // M (A) or N (B): logical extent along the tile rows
   bool edge = false;      // some loads fall outside the operand (padded tiles)
   bool user_lds = false;  // LDS layout given by the caller
@@ -248,11 +250,50 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   LayoutP FA = mfma_fragment_layout(MB == 32 ? 0 : 1, 0);
   LayoutP FC = mfma_fragment_layout(MB == 32 ? 0 : 1, 2);
 
+  // Row of fragment row r of MFMA block mi inside the wave tile: block mi
+  // covers rows mi*MB .. mi*MB+MB-1, or with row pairs (mpair) blocks 2m and
+  // 2m+1 take the even and the odd rows of rows 2m*MB .. 2m*MB+2MB-1, so that
+  // one lane holds two adjacent rows (the two rows of a Z-order block).
+  auto wrow = [&](Ctx& c, bool mpair, const Sum& mi, const Sum& r) -> Sum {
+    if (mpair) return add(c, add(c, mulc(c, fdiv(c, mi, 2), 2 * MB), mulc(c, r, 2)), fmod(c, mi, 2));
+    return add(c, mulc(c, mi, MB), r);
+  };
   // How a wave reads its MFMA fragments of operand `o` from its LDS layout:
   // one 16-byte vector per lane, the transposing load, 4 dwords of two
   // consecutive k each, or element by element.
   auto frag_modes = [&](Operand& o) {
-    o.frvec = o.frtr = o.frdw = false;
+    o.frvec = o.frtr = o.frdw = o.frzp = false;
+    if (o.mpair) {
+      // Row pairs: a lane's fragments of blocks 2m and 2m+1 (rows 2r and
+      // 2r+1) from two 16-byte reads (h = 0, 1): element e = 4h + 2t + q of
+      // block 2m + p lies at read h's offset + 4t + 2p + q, the offset a
+      // multiple of 8 (a 2 x 4 Z block per 16-byte slot).
+      Ctx c;
+      int lane = c.var("lane", 64), w = c.var("w", NWAVES), m = c.var("m", MI / 2), pp = c.var("p", 2),
+          s = c.var("s", bk / KB), h = c.var("h", 2), t = c.var("t", 2), q = c.var("q", 2);
+      SymAlg al{&c};
+      Sum mi = add(c, mulc(c, var(c, m), 2), var(c, pp));
+      Sum e = add(c, add(c, mulc(c, var(c, h), 4), mulc(c, var(c, t), 2)), var(c, q));
+      Sum f = FA->apply(al, {var(c, lane), e});
+      Sum r = fdiv(c, f, KB), k = fmod(c, f, KB);
+      Sum wpos = fdiv(c, var(c, w), NWN);
+      Sum row = add(c, mulc(c, wpos, wm), wrow(c, true, mi, r));
+      Sum kk = add(c, mulc(c, var(c, s), KB), k);
+      const Sum off = o.lds->apply(al, {row, kk});
+      Sum dep, rest;
+      if (split_by(off, {q, pp, t}, &dep, &rest) && dep.c0 == 0 && dep.t.size() == 3 &&
+          known_multiple(rest) % 8 == 0) {
+        bool ok = true;
+        for (const Term& tm : dep.t) {
+          const Atom& a = *tm.a;
+          const i64 want = a.var == q ? 1 : (a.var == pp ? 2 : 4);
+          ok = ok && a.op == Op::Field && a.a == 1 && a.b == 0 && (a.var == q || a.var == pp || a.var == t) &&
+               tm.c == want;
+        }
+        o.frzp = ok;
+      }
+      return;
+    }
     // Vector fragment read?
     {
       Ctx c;
@@ -262,7 +303,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
       Sum f = FA->apply(al, {var(c, lane), var(c, e)});
       Sum r = fdiv(c, f, KB), k = fmod(c, f, KB);
       Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
-      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+      Sum row = add(c, mulc(c, wpos, o.is_b ? wn : wm), wrow(c, o.mpair, var(c, mi), r));
       Sum kk = add(c, mulc(c, var(c, s), KB), k);
       o.frvec = contiguous_in(o.lds->apply(al, {row, kk}), e, 8);
     }
@@ -303,7 +344,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
       Sum f = FA->apply(al, {var(c, lane), e});
       Sum r = fdiv(c, f, KB), k = fmod(c, f, KB);
       Sum wpos = o.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
-      Sum row = add(c, add(c, mulc(c, wpos, o.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+      Sum row = add(c, mulc(c, wpos, o.is_b ? wn : wm), wrow(c, o.mpair, var(c, mi), r));
       Sum kk = add(c, mulc(c, var(c, s), KB), k);
       const Sum off = o.lds->apply(al, {row, kk});
       o.frdw = contiguous_in(off, q, 2);
@@ -495,6 +536,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
   // directly into the z_lds layout, which keeps each block in one LDS slot;
   // a lane then reads its row's 8 k as 4 dwords (2 k each).
   LayoutP zl[2];
+  bool zpair[2] = {false, false};
   for (int k = 0; k < 2; ++k) {
     const Operand& o = ops[k];
     if (o.user_lds || o.axis != 2 || o.VR != 2 || o.VC != 4 || o.bdi != std::vector<i64>{0, 1, 0} ||
@@ -502,6 +544,16 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
       continue;
     Operand t = o;
     t.lds = z_lds(o.R, o.KD);
+    if (!o.is_b && MI % 2 == 0 && tune("gemm.zpair", 1)) {
+      t.mpair = true;
+      frag_modes(t);
+      if (t.frzp) {
+        zl[k] = t.lds;
+        zpair[k] = true;
+        continue;
+      }
+      t.mpair = false;
+    }
     frag_modes(t);
     if (t.frdw) zl[k] = t.lds;
   }
@@ -539,6 +591,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
       Operand& o = ops[k];
       if (zl[k]) {
         o.lds = zl[k];
+        o.mpair = zpair[k];
         frag_modes(o);
       }
       o.direct = true;
@@ -680,7 +733,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
                      Sum f0 = FA->apply(al, {var(c, lane), var(c, e)});
                      Sum r = fdiv(c, f0, KB), kq = fmod(c, f0, KB);
                      Sum wpos = oo.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
-                     Sum row = add(c, add(c, mulc(c, wpos, oo.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+                     Sum row = add(c, mulc(c, wpos, oo.is_b ? wn : wm), wrow(c, oo.mpair, var(c, mi), r));
                      Sum kk = add(c, mulc(c, var(c, s), KB), kq);
                      FnSpec f;
                      f.params = {lane, w, mi, s, e};
@@ -701,6 +754,24 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
                        f.outs = {in_range(c, oo, var(c, tt), var(c, kt), i, j)};
                        return f;
                      }});
+    if (o.frzp)
+      fns.push_back({p + "fz", [&, k](Ctx& c) {
+                       // LDS offset of the 16-byte read h of the fragment pair
+                       // (blocks 2m, 2m+1): fragment element 4h of block 2m.
+                       const Operand& oo = ops[k];
+                       int lane = c.var("lane", 64), w = c.var("w", NWAVES), m = c.var("m", MI / 2),
+                           s = c.var("s", bk / KB), h = c.var("h", 2);
+                       SymAlg al{&c};
+                       Sum f0 = FA->apply(al, {var(c, lane), mulc(c, var(c, h), 4)});
+                       Sum r = fdiv(c, f0, KB), kq = fmod(c, f0, KB);
+                       Sum wpos = fdiv(c, var(c, w), NWN);
+                       Sum row = add(c, mulc(c, wpos, wm), wrow(c, true, mulc(c, var(c, m), 2), r));
+                       Sum kk = add(c, mulc(c, var(c, s), KB), kq);
+                       FnSpec f;
+                       f.params = {lane, w, m, s, h};
+                       f.outs = {oo.lds->apply(al, {row, kk})};
+                       return f;
+                     }});
     if (o.frdw && o.frdw_d)
       fns.push_back({p + "fd", [&, k](Ctx& c) {
                        // LDS offset of fragment element 4h: the first dword of
@@ -712,7 +783,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
                        Sum f0 = FA->apply(al, {var(c, lane), mulc(c, var(c, h), 4)});
                        Sum r = fdiv(c, f0, KB), kq = fmod(c, f0, KB);
                        Sum wpos = oo.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
-                       Sum row = add(c, add(c, mulc(c, wpos, oo.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+                       Sum row = add(c, mulc(c, wpos, oo.is_b ? wn : wm), wrow(c, oo.mpair, var(c, mi), r));
                        Sum kk = add(c, mulc(c, var(c, s), KB), kq);
                        FnSpec f;
                        f.params = {lane, w, mi, s, h};
@@ -733,7 +804,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
                        Sum f0 = FA->apply(al, {lp, ep});
                        Sum r = fdiv(c, f0, KB), kq = fmod(c, f0, KB);
                        Sum wpos = oo.is_b ? fmod(c, var(c, w), NWN) : fdiv(c, var(c, w), NWN);
-                       Sum row = add(c, add(c, mulc(c, wpos, oo.is_b ? wn : wm), mulc(c, var(c, mi), MB)), r);
+                       Sum row = add(c, mulc(c, wpos, oo.is_b ? wn : wm), wrow(c, oo.mpair, var(c, mi), r));
                        Sum kk = add(c, mulc(c, var(c, s), KB), kq);
                        FnSpec f;
                        f.params = {lane, w, mi, s, h};
@@ -753,7 +824,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
     Sum f0 = FC->apply(al, {var(c, *lane), var(c, *r)});
     Sum row = fdiv(c, f0, MB), col = fmod(c, f0, MB);
     Sum m = add(c, add(c, mulc(c, var(c, *tm), bm), mulc(c, fdiv(c, var(c, *w), NWN), wm)),
-                add(c, mulc(c, var(c, *mi), MB), row));
+                wrow(c, ops[0].mpair, var(c, *mi), row));
     Sum n = add(c, add(c, mulc(c, var(c, *tn), bn), mulc(c, fmod(c, var(c, *w), NWN), wn)),
                 add(c, mulc(c, var(c, *ni), MB), col));
     return LC->apply(al, {m, n});
@@ -767,7 +838,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
                      Sum f0 = FC->apply(al, {var(c, lane), var(c, r)});
                      Sum row = fdiv(c, f0, MB), col = fmod(c, f0, MB);
                      Sum m = add(c, add(c, mulc(c, var(c, tm), bm), mulc(c, fdiv(c, var(c, w), NWN), wm)),
-                                 add(c, mulc(c, var(c, mi), MB), row));
+                                 wrow(c, ops[0].mpair, var(c, mi), row));
                      Sum n = add(c, add(c, mulc(c, var(c, tn), bn), mulc(c, fmod(c, var(c, w), NWN), wn)),
                                  add(c, mulc(c, var(c, ni), MB), col));
                      FnSpec f;
@@ -836,6 +907,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
       << "SEP " << (o.sep ? 1 : 0) << "\n#define " << P2[k] << "SVEC " << (o.svec ? 1 : 0) << "\n#define " << P2[k]
       << "FRVEC " << (o.frvec ? 1 : 0) << "\n#define " << P2[k] << "FRTR " << (o.frtr ? 1 : 0) << "\n#define " << P2[k]
       << "FRDW " << (o.frdw ? 1 : 0) << "\n#define " << P2[k] << "FRDW_D " << o.frdw_d << "\n#define " << P2[k]
+      << "FRZP " << (o.frzp ? 1 : 0) << "\n#define " << P2[k]
       << "NVEC " << o.NVEC << "u\n#define " << P2[k]
       << "GUARD " << (o.guard ? 1 : 0) << "\n#define " << P2[k] << "EDGE " << (o.edge ? 1 : 0) << "\n#define "
       << P2[k] << "BUF " << (o.direct && 2 * o.glob->phys_size() < (i64(1) << 31) ? 1 : 0) << "\n#define "
@@ -917,7 +989,7 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
        << MB << "x" << KB << " sched" << (xcd ? "+xcd" : "") << " A:V" << ops[0].V
        << (ops[0].gaxis == 2 ? "b" + std::to_string(ops[0].VR) + "x" + std::to_string(ops[0].VC) : (ops[0].gaxis ? "k" : "m"))
        << (ops[0].sep ? " sep" : " full") << (ops[0].svec ? " svec" : " sscalar")
-       << (ops[0].frvec ? " frvec" : (ops[0].frtr ? " frtr" : (ops[0].frdw ? " frdw" : " frscalar"))) << " B:V" << ops[1].V
+       << (ops[0].frvec ? " frvec" : (ops[0].frtr ? " frtr" : (ops[0].frzp ? " frzpair" : (ops[0].frdw ? " frdw" : " frscalar")))) << " B:V" << ops[1].V
        << (ops[1].gaxis == 2 ? "b" + std::to_string(ops[1].VR) + "x" + std::to_string(ops[1].VC) : (ops[1].gaxis ? "k" : "n"))
        << (ops[1].sep ? " sep" : " full") << (ops[1].svec ? " svec" : " sscalar")
        << (ops[1].frvec ? " frvec" : (ops[1].frtr ? " frtr" : (ops[1].frdw ? " frdw" : " frscalar"))) << (csep ? " C:sep" : " C:full") << (wide ? " i64" : " u32")

@@ -31,6 +31,9 @@
 //                                    elements 2p and 2p + 1 adjacent in LDS;
 //   A_FRDW_D, a_fd(lane, w, mi, s, h)  with A_FRDW_D > 0, dword 2h at a_fd(h)
 //                                    and dword 2h + 1 A_FRDW_D elements on
+//   A_FRZP, a_fz(lane, w, m, s, h)   MFMA blocks 2m, 2m+1 hold the even and odd
+//                                    rows of a band; a lane reads both from two
+//                                    16-byte slots at a_fz(h), h = 0, 1
 //   (b_* likewise with tn)
 //   c_t(tm, tn) c_l(lane, w, mi, ni, r)   or   c_f(tm, tn, lane, w, mi, ni, r)
 //   A_BUF (and B_BUF): direct copies are range-checked buffer loads with
@@ -81,8 +84,8 @@ LEGO_FN mf_t lds_frag(const elem_t* base, IDX_T off) {
 // Fragment as 4 dwords, each 2 consecutive k of the lane's row (Z-order
 // operands, whose LDS slots interleave two rows); reads whose offsets differ
 // by a constant pair up into ds_read2_b32.
+typedef unsigned u4_t __attribute__((ext_vector_type(4)));
 LEGO_FN mf_t lds_frag_dw(const elem_t* base, IDX_T o0, IDX_T o1, IDX_T o2, IDX_T o3) {
-  typedef unsigned u4_t __attribute__((ext_vector_type(4)));
   const u4_t t = {*(const unsigned*)(base + o0), *(const unsigned*)(base + o1), *(const unsigned*)(base + o2),
                   *(const unsigned*)(base + o3)};
   return __builtin_bit_cast(mf_t, t);
@@ -158,7 +161,7 @@ LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
 // FRAG_DIST.
 static_assert(FRAG_DIST == 1 || (FRAG_DIST < BK / KB && NFB > FRAG_DIST), "fragment sets");
 // LDS read instructions per fragment.
-#define A_FRD (A_FRTR ? 2 : (A_FRVEC ? 1 : (A_FRDW ? 2 : 8)))
+#define A_FRD (A_FRTR ? 2 : (A_FRVEC || A_FRZP ? 1 : (A_FRDW ? 2 : 8)))
 #define B_FRD (B_FRTR ? 2 : (B_FRVEC ? 1 : (B_FRDW ? 2 : 8)))
 #define FRAG_READS (MI * A_FRD + NI * B_FRD)
 
@@ -330,6 +333,15 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       af[buf][i] = lds_frag_tr(la, a_ft(lane, w, i, s, 0), a_ft(lane, w, i, s, 1));
 #elif A_FRVEC
       af[buf][i] = lds_frag(la, a_fr(lane, w, i, s, 0));
+#elif A_FRZP
+      // Row pairs: blocks i and i + 1 hold the even and the odd rows of a
+      // band, and two 16-byte reads bring a lane both rows' 8 k (a slot is
+      // one 2 x 4 Z block); the registers keep the slots as read (a_op picks
+      // the operands).  The odd block is read with its even partner.
+      if (i % 2 == 0) {
+        af[buf][i] = lds_frag(la, a_fz(lane, w, i / 2, s, 0));
+        af[buf][i + 1] = lds_frag(la, a_fz(lane, w, i / 2, s, 1));
+      }
 #elif A_FRDW && A_FRDW_D
       {
         const IDX_T o0 = a_fd(lane, w, i, s, 0), o1 = a_fd(lane, w, i, s, 1);
@@ -373,9 +385,24 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // Row r of the MFMAs of one substep with fragment set fb: every MFMA of a
   // row has the same first operand, A's fragment r.
 #define MFMA_ROWS MI
+  // The A operand of MFMA block row r.  With row pairs (A_FRZP) the
+  // fragment registers of blocks 2m, 2m+1 hold the two 16-byte slots as read
+  // (dwords: row 2r at k, k+1; row 2r+1 at k, k+1; then k+2, k+3), and the
+  // operand is picked out here, when the MFMAs use it, so the register moves
+  // never wait for the reads.
+  auto a_op = [&](int r, int fb) -> mf_t {
+#if A_FRZP
+    const u4_t x0 = __builtin_bit_cast(u4_t, af[fb][r & ~1]), x1 = __builtin_bit_cast(u4_t, af[fb][r | 1]);
+    const int p = r & 1;
+    return __builtin_bit_cast(mf_t, (u4_t){x0[p], x0[p + 2], x1[p], x1[p + 2]});
+#else
+    return af[fb][r];
+#endif
+  };
   auto mfma_row = [&](int r, int fb) {
+    const mf_t a = a_op(r, fb);
 #pragma unroll
-    for (int j = 0; j < NI; ++j) acc[r][j] = MFMA(af[fb][r], bf[fb][j], acc[r][j]);
+    for (int j = 0; j < NI; ++j) acc[r][j] = MFMA(a, bf[fb][j], acc[r][j]);
   };
   auto mfma_all = [&](int fb) {
 #pragma unroll

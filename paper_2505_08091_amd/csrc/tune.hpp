@@ -3,7 +3,7 @@
 // only; it is read once per process, is not part of the C ABI, and every
 // default is what the measurements chose).  Keys: gemm.lds_s, gemm.mfma,
 // gemm.direct, gemm.prefetch, gemm.rolling, gemm.dma_spread, gemm.frag_dist,
-// gemm.frag_spread, gemm.store_at, gemm.persist, gemm.ring_unroll, gemm.wide_waves, gemm.zdirect,
+// gemm.frag_spread, gemm.store_at, gemm.persist, gemm.ring_unroll, gemm.wide_waves, gemm.zdirect, gemm.zpair,
 // gemm.dma_rows, index.nt_store, index.grid, remap.nontemporal, remap.box,
 // remap.box_side, remap.box_tile, remap.box_band, remap.nt, remap.unroll, remap.order (0 destination, 1
 // source), remap.xcd, remap.persist, remap.tile_bytes, remap.block (LDS block

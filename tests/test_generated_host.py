@@ -409,6 +409,19 @@ int main() {
 #endif
     }
 #endif
+  // row-pair fragment reads: element 4h + 2t + q of block 2m + p at
+  // a_fz(m, h) + 4t + 2p + q, a_fz a multiple of 8
+#if A_FRZP
+  for (u64 w = 0; w < NWAVES; ++w)
+    for (u64 s = 0; s < BK / KB; ++s) for (u64 l = 0; l < 64; ++l) for (u64 m = 0; m < MI / 2; ++m)
+      for (u64 h = 0; h < 2; ++h) {
+        u64 z = a_fz((IDX_T)l, (IDX_T)w, (IDX_T)m, (IDX_T)s, (IDX_T)h);
+        if (z % 8 || z + 8 > BM * BK) FAIL("a_fz misaligned or out of range");
+        for (u64 p = 0; p < 2; ++p) for (u64 t = 0; t < 2; ++t) for (u64 q = 0; q < 2; ++q)
+          if ((u64)a_fr((IDX_T)l, (IDX_T)w, (IDX_T)(2 * m + p), (IDX_T)s, (IDX_T)(4 * h + 2 * t + q)) != z + 4 * t + 2 * p + q)
+            FAIL("a_fz mismatch");
+      }
+#endif
   // epilogue: every C element written exactly once
   {
     std::vector<char> c(GEMM_M * GEMM_N);
@@ -618,7 +631,7 @@ def _gemm_cases():
     return cases
 
 
-N_GEMM_CASES = 45
+N_GEMM_CASES = 46
 
 
 def test_gemm_case_count():

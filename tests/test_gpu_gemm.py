@@ -226,25 +226,29 @@ def test_gemm_c5_morton_a(lego):
 
 def _morton_direct_cases(L):
     """Morton-order A copied directly into LDS (each 2 x 4 Z block in one
-    slot) and read as dword pairs: bf16 with column-major B, smaller tiles
-    with row-major B (the transposing read beside it), 32-deep k-steps, and a
-    workgroup walking several tiles."""
+    slot).  With an even number of MFMA blocks per wave along m, blocks 2m
+    and 2m+1 take the even and odd rows of a band and a lane reads both rows
+    of its blocks (`frzpair`: the C rows follow the same order); otherwise a
+    lane reads its row as dword pairs (`frdw`).  bf16 with column-major B,
+    smaller tiles with row-major B (the transposing read beside it), 32-deep
+    k-steps, a workgroup walking several tiles, and one-block-high wave tiles."""
     return [
-        dict(M=1024, N=1024, K=1024, dtype="bf16", bl="Col"),
-        dict(M=1024, N=512, K=2048, dtype="f16", bl="Row", bm=128, bn=128, bk=64, wm=64, wn=64),
-        dict(M=512, N=512, K=512, dtype="f16", bl="Col", bm=128, bn=128, bk=32, wm=64, wn=64),
-        dict(M=1024, N=1024, K=512, dtype="f16", bl="Row", max_workgroups=5),
+        dict(M=1024, N=1024, K=1024, dtype="bf16", bl="Col", mode="frzpair"),
+        dict(M=1024, N=512, K=2048, dtype="f16", bl="Row", bm=128, bn=128, bk=64, wm=64, wn=64, mode="frzpair"),
+        dict(M=512, N=512, K=512, dtype="f16", bl="Col", bm=128, bn=128, bk=32, wm=64, wn=64, mode="frzpair"),
+        dict(M=1024, N=1024, K=512, dtype="f16", bl="Row", max_workgroups=5, mode="frzpair"),
+        dict(M=512, N=512, K=512, dtype="bf16", bl="Col", bm=64, bn=128, bk=64, wm=32, wn=64, mode="frdw"),
     ]
 
 
 def _morton_direct_kw(L, case):
-    kw = {k: v for k, v in case.items() if k not in ("bl",)}
+    kw = {k: v for k, v in case.items() if k not in ("bl", "mode")}
     kw["a"] = L.as_layout(L.GenP("morton", [case["M"], case["K"]]))
     kw["b"] = L.as_layout(getattr(L, case["bl"])(case["K"], case["N"]))
     return kw
 
 
-@pytest.mark.parametrize("i", range(4))
+@pytest.mark.parametrize("i", range(5))
 def test_gemm_morton_a_direct(lego, i):
     """Morton-A GEMMs on the direct-copy path with dword fragment reads,
     every output element against the fp64 oracle reading A through its
@@ -260,7 +264,7 @@ def test_gemm_morton_a_direct(lego, i):
     a_mz = torch.from_numpy(a_mz_bits.view(np.int16).copy()).view(a_log.dtype)
     plan = lego.gemm_plan(M, N, K, dt, **{k: v for k, v in kw.items() if k != "max_workgroups"})
     say(f"gemm Morton-A direct {case} plan={plan}")
-    assert "frdw" in plan and "direct-lds" in plan, plan
+    assert f" {case['mode']} " in plan and "direct-lds" in plan, plan
     c = _run(lego, a_mz, b, M, N, K, dt, **kw).reshape(M, N)
     assert np.isfinite(c).all()
     r = OG.gemm(a_mz_bits, S.as_numpy_bits(b), omz, OL.as_layout(getattr(OL, case["bl"])(K, N)), dt)
