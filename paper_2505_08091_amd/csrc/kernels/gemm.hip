@@ -684,6 +684,13 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // The stage of the current tile's step 0 (the ring advances KT steps per
   // tile).
   IDX_T stage0 = 0;
+  // The k-loop's trip count is hidden from the compiler.  Unrolled in full
+  // (K of two or three steps), the steps and the next tile's set-up become
+  // one straight-line block whose register demand spilled, and the fragment
+  // reads of the last step, dead there, shared registers with live values
+  // while still in flight.
+  IDX_T kt_end = KT;
+  asm volatile("" : "+s"(kt_end));
   for (;;) {
     const IDX_T npid = pid + (IDX_T)gridDim.x;
     const bool has_next = PERSIST && npid < ntiles;
@@ -696,7 +703,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       // each step's stage is a constant and its fragment addresses are
       // loop-invariant registers (1.6% on the 8192^3 bf16 GEMM; plans with
       // two waves per SIMD lack the registers for them).
-      for (IDX_T kt = 0; kt < KT; kt += NSTAGES) {
+      for (IDX_T kt = 0; kt < kt_end; kt += NSTAGES) {
 #pragma unroll
         for (int p = 0; p < NSTAGES; ++p) {
           const bool own = kt + p + NSTAGES < KT;
@@ -704,7 +711,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
         }
       }
     } else {
-      for (IDX_T kt = 0; kt < KT; ++kt) {
+      for (IDX_T kt = 0; kt < kt_end; ++kt) {
         const bool own = kt + NSTAGES < KT;
         kstep((int)((stage0 + kt) % NSTAGES), own ? cur : nxt, (kt + NSTAGES) % KT);
       }

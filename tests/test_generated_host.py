@@ -628,10 +628,12 @@ def _gemm_cases():
     cases += [{k: v for k, v in c.items() if k not in ("oa", "ob", "max_workgroups")} for c in _persistent_cases(L)]
     from tests.test_gpu_gemm import _morton_direct_cases, _morton_direct_kw
     cases += [{k: v for k, v in _morton_direct_kw(L, c).items() if k != "max_workgroups"} for c in _morton_direct_cases(L)]
+    from tests.test_gpu_gemm import _random_cases
+    cases += [{k: v for k, v in c.items() if k not in ("oa", "ob", "max_workgroups")} for c in _random_cases(L)]
     return cases
 
 
-N_GEMM_CASES = 46
+N_GEMM_CASES = 70
 
 
 def test_gemm_case_count():

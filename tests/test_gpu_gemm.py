@@ -365,6 +365,71 @@ def test_gemm_ragged_sizes(lego, i):
     assert ok, (mre, fre)
 
 
+def _random_cases(L):
+    """24 GEMM configurations drawn from a fixed seed: fp16 or bf16; A
+    row-major, column-major or in Morton order (power-of-two M and K), B row-
+    or column-major; the default tiles or one of six smaller tile and wave
+    shapes; ragged sizes unless A is in Morton order; and now and then a
+    workgroup cap, so that workgroups walk several tiles.  Configurations the
+    planner rejects are drawn again."""
+    rng = np.random.default_rng(2505)
+    tiles = [None, (128, 128, 64, 64, 64), (128, 128, 32, 64, 64), (64, 64, 32, 32, 32), (64, 128, 64, 32, 64),
+             (256, 128, 64, 128, 64), (128, 256, 64, 64, 128)]
+    out = []
+    while len(out) < 24:
+        dt = ("f16", "bf16")[rng.integers(2)]
+        la, lb = ("Row", "Col", "Morton")[rng.integers(3)], ("Row", "Col")[rng.integers(2)]
+        if la == "Morton":
+            M, K = (int(x) for x in 2 ** rng.integers(6, 10, 2))
+        else:
+            M, K = (int(x) for x in rng.integers(1, 700, 2))
+        N = int(rng.integers(1, 700))
+        if rng.integers(2):  # whole tiles: the plan may walk tiles (persistent)
+            N = 256 * int(rng.integers(1, 3))
+            if la != "Morton":
+                M, K = 256 * int(rng.integers(1, 3)), 256 * int(rng.integers(1, 3))
+        kw = dict(M=M, N=N, K=K, dtype=dt)
+        t = tiles[rng.integers(len(tiles))]
+        if t:
+            kw.update(bm=t[0], bn=t[1], bk=t[2], wm=t[3], wn=t[4])
+        if la == "Morton":
+            kw["a"], kw["oa"] = L.as_layout(L.GenP("morton", [M, K])), OL.as_layout(OL.morton_genp(M, K))
+        else:
+            kw["a"], kw["oa"] = L.as_layout(getattr(L, la)(M, K)), OL.as_layout(getattr(OL, la)(M, K))
+        kw["b"], kw["ob"] = L.as_layout(getattr(L, lb)(K, N)), OL.as_layout(getattr(OL, lb)(K, N))
+        try:
+            L.gemm_plan(M, N, K, dt, **{k: v for k, v in kw.items() if k not in ("M", "N", "K", "dtype", "oa", "ob")})
+        except L.LegoError:
+            continue
+        if rng.integers(3) == 0:
+            kw["max_workgroups"] = int(rng.integers(1, 8))
+        out.append(kw)
+    return out
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_gemm_random_configs(lego, i):
+    """Every output element of a seeded random GEMM configuration against the
+    fp64 oracle (C pre-filled with NaN)."""
+    kw = dict(_random_cases(lego)[i])
+    M, N, K, dtype = kw.pop("M"), kw.pop("N"), kw.pop("K"), kw.pop("dtype")
+    oa, ob = kw.pop("oa"), kw.pop("ob")
+    a_log = S.tensor(M * K, dtype, seed=S.SEED_A)
+    b_log = S.tensor(K * N, dtype, seed=S.SEED_B)
+    # operands stored in their layouts by the oracle's remap of row-major values
+    a_bits = OR.remap(OL.as_layout(OL.Row(M, K)), oa, S.as_numpy_bits(a_log))
+    b_bits = OR.remap(OL.as_layout(OL.Row(K, N)), ob, S.as_numpy_bits(b_log))
+    import torch
+    a = torch.from_numpy(a_bits.view(np.int16).copy()).view(a_log.dtype)
+    b = torch.from_numpy(b_bits.view(np.int16).copy()).view(b_log.dtype)
+    say(f"gemm random {i}: {M}x{N}x{K} {dtype} plan={lego.gemm_plan(M, N, K, dtype, **{k: v for k, v in kw.items() if k != 'max_workgroups'})}")
+    c = _run(lego, a, b, M, N, K, dtype, **kw).reshape(M, N)
+    assert np.isfinite(c).all()
+    r = OG.gemm(a_bits, b_bits, oa, ob, dtype)
+    ok, mre, fre = OG.check_tolerance(c, r)
+    assert ok, (mre, fre)
+
+
 def _persistent_cases(L):
     """GEMMs whose workgroups each walk several output tiles (the plan is
     persistent and max_workgroups is below the tile count), so the LDS ring
