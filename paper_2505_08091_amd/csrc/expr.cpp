@@ -357,7 +357,19 @@ Sum fmod(const Ctx& c, const Sum& x, i64 n) {
   return mod_atom(c, L, n);
 }
 
-Sum bxor(const Ctx& c, const Sum& x, const Sum& y) {
+// max(x, 0), as select(x < 0, 0, x).  XOR and the integer square root are
+// only defined here for non-negative operands; where the interval analysis
+// cannot show that (it loses the correlation between the terms of, e.g., the
+// triangle offset y - d(d+1)/2 of an antidiagonal inverse) but the operand is
+// a coordinate, which is never negative for an index in range, the operand is
+// clamped, a no-op on every index in range.
+static Sum clamp0(const Ctx& c, const Sum& x) {
+  if (range(x).lo >= 0) return x;
+  return select(c, lt(c, x, cst(0)), cst(0), x);
+}
+
+Sum bxor(const Ctx& c, const Sum& x0, const Sum& y0) {
+  const Sum x = clamp0(c, x0), y = clamp0(c, y0);
   if (x.is_const() && y.is_const()) return cst(x.c0 ^ y.c0);
   if (x.is_const() && x.c0 == 0) return y;
   if (y.is_const() && y.c0 == 0) return x;
@@ -414,11 +426,17 @@ Sum select(const Ctx& c, const Sum& cond, const Sum& x, const Sum& y) {
   }
   if (!common.t.empty()) return add(c, common, select(c, cond, xr, yr));
   Interval rx = range(x), ry = range(y);
-  return atom_sum(make_op(Op::Select, {cond, x, y}, 0, {std::min(rx.lo, ry.lo), std::max(rx.hi, ry.hi)}));
+  Interval r{std::min(rx.lo, ry.lo), std::max(rx.hi, ry.hi)};
+  // select(y < 0, 0, y) is max(y, 0): never negative
+  if (x.is_const() && x.c0 == 0 && cond.c0 == 0 && cond.t.size() == 1 && cond.t[0].c == 1 &&
+      cond.t[0].a->op == Op::Lt && cond.t[0].a->kids[1].is_const() && cond.t[0].a->kids[1].c0 == 0 &&
+      skey(cond.t[0].a->kids[0]) == skey(y))
+    r.lo = std::max<i64>(r.lo, 0);
+  return atom_sum(make_op(Op::Select, {cond, x, y}, 0, r));
 }
 
-Sum isqrt(const Ctx& c, const Sum& x) {
-  (void)c;
+Sum isqrt(const Ctx& c, const Sum& x0) {
+  const Sum x = clamp0(c, x0);
   if (x.is_const()) return cst(isqrt_exact(x.c0));
   Interval r = range(x);
   if (r.lo < 0) throw std::invalid_argument("isqrt of a possibly negative value");
@@ -508,9 +526,12 @@ bool split_by(const Sum& s, const std::vector<int>& group, Sum* in_group, Sum* r
 
 bool digits_of(const Ctx& c, const Sum& s, int v, std::vector<Digit>* out) {
   out->clear();
+  // A digit permutation has no constant and positive digit weights (a map
+  // such as n - 1 - p, a reversal, is a bijection but not of this form).
+  if (s.c0 != 0) return false;
   for (auto& t : s.t) {
     const Atom& a = *t.a;
-    if (a.op != Op::Field || a.var != v) return false;
+    if (a.op != Op::Field || a.var != v || t.c <= 0) return false;
     i64 b = a.b ? a.b : (c.vars[v].hi / a.a + 1);
     out->push_back({a.a, b, t.c});
   }

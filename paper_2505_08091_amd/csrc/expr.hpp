@@ -104,8 +104,9 @@ Sum subst(const Ctx& c, const Sum& s, int v, const Sum& repl);
 // group (the expression is not additively separable).
 bool split_by(const Sum& s, const std::vector<int>& group, Sum* in_group, Sum* rest);
 
-// Digit structure of a pure field sum: every atom is a Field of one variable
-// and the fields of that variable tile its digits without overlap.
+// Digit structure of a pure field sum: no constant, every atom a Field of one
+// variable with a positive weight, and the fields of that variable tile its
+// digits without overlap.
 struct Digit {
   i64 a, b, coeff;  // (v / a) % b contributes coeff * digit
 };

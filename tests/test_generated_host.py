@@ -571,6 +571,22 @@ def test_remap_sources_of_gpu_cases(elem_bytes):
                 assert (perm == exp).all(), (name, elem_bytes)
 
 
+@pytest.mark.parametrize("i", range(24))
+def test_remap_sources_of_random_cases(i):
+    """The seeded random remaps of the GPU tests, both directions, on the host."""
+    import paper_2505_08091_amd as L
+    from tests.test_gpu_remap import _random_remap_cases
+    name, ls, ld, ols, old, elem = _random_remap_cases(L)[i]
+    with tempfile.TemporaryDirectory() as tmp:
+        out = os.path.join(tmp, "out.bin")
+        for a, b, oa, ob in ((ls, ld, ols, old), (ld, ls, old, ols)):
+            src = L.plan_source("remap", a, b, param=elem)
+            _compile_and_run(src, HARNESS_REMAP, tmp, [out])
+            perm = np.fromfile(out, dtype=np.int64)
+            exp = OR.remap(oa, ob, np.arange(1, OR.phys_size(oa) + 1, dtype=np.int64)) - 1
+            assert (perm == exp).all(), name
+
+
 def _huge_remap_cases():
     """Remaps of 65600^2 one-byte elements (more than 2^32, so byte and element
     offsets need 64 bits; 65600 = 64 * 1025 has odd factors)."""

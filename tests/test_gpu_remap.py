@@ -205,6 +205,91 @@ def _small_cases(L):
     ]
 
 
+def _random_piece(L, rng, r, c):
+    """A random permutation piece over [r, c] (and its oracle twin): row- or
+    column-major, reversal, an XOR swizzle (c a power of two), Morton order
+    (powers of two) or the antidiagonal order (square)."""
+    pow2 = lambda x: x & (x - 1) == 0
+    kinds = ["row", "col", "reverse"]
+    if pow2(c) and c >= 2:
+        kinds.append("xor")
+    if pow2(r) and pow2(c):
+        kinds.append("morton")
+    if r == c:
+        kinds.append("antidiag")
+    k = kinds[rng.integers(len(kinds))]
+    if k == "row":
+        return L.Row(r, c), OL.Row(r, c)
+    if k == "col":
+        return L.Col(r, c), OL.Col(r, c)
+    if k == "reverse":
+        return L.GenP("reverse", [r, c]), OL.reverse_genp(r, c)
+    if k == "xor":
+        v = int(2 ** rng.integers(0, int(np.log2(c)) + 1))
+        sh = int(rng.integers(1, 5))
+        return L.GenP("xor_swizzle", [r, c], [v, sh]), OL.xor_swizzle_genp(r, c, v, sh)
+    if k == "morton":
+        return L.GenP("morton", [r, c]), OL.morton_genp(r, c)
+    return L.GenP("antidiag", [r, r]), OL.antidiag_genp(r)
+
+
+def _random_layout(L, rng, R, C, tiles):
+    """A whole layout over [R, C]: one piece, or TileOrderBy over the given
+    tile shapes (each level a random piece)."""
+    if not tiles:
+        lp, op = _random_piece(L, rng, R, C)
+        return L.as_layout(lp), OL.as_layout(op)
+    dims = [(R // int(np.prod([t[0] for t in tiles])), C // int(np.prod([t[1] for t in tiles])))] + tiles
+    ps = [_random_piece(L, rng, a, b) for a, b in dims]
+    return L.TileOrderBy(*[p[0] for p in ps]), OL.TileOrderBy(*[p[1] for p in ps])
+
+
+def _random_remap_cases(L):
+    """24 remaps between random layouts of one logical shape, from a fixed
+    seed: shapes of 1 to 3 tile levels whose tiles are small powers of two or
+    odd sizes, each level a random piece (row/column-major, reversal, XOR
+    swizzle, Morton, antidiagonal), element sizes of 1, 2, 4 and 8 bytes."""
+    rng = np.random.default_rng(8091)
+    sizes = [1, 2, 3, 4, 5, 7, 8, 16, 32, 64]
+    out = []
+    while len(out) < 24:
+        levels = int(rng.integers(0, 3))
+        tiles = [(sizes[rng.integers(len(sizes))], sizes[rng.integers(len(sizes))]) for _ in range(levels)]
+        outer = (int(rng.integers(1, 40)), int(rng.integers(1, 40)))
+        if rng.integers(3) == 0:
+            outer = (int(2 ** rng.integers(0, 6)),) * 2
+        R = outer[0] * int(np.prod([t[0] for t in tiles]))
+        C = outer[1] * int(np.prod([t[1] for t in tiles]))
+        if R * C > (1 << 22) or R * C < 2:
+            continue
+        # the source side may tile differently from the destination
+        tiles_b = tiles if rng.integers(2) else []
+        ls, ols = _random_layout(L, rng, R, C, tiles)
+        ld, old = _random_layout(L, rng, R, C, tiles_b)
+        elem = int((1, 2, 4, 8)[rng.integers(4)])
+        out.append((f"random {len(out)}: {R}x{C} tiles {tiles}/{tiles_b} {elem} B", ls, ld, ols, old, elem))
+    return out
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_remap_random_layouts(lego, i):
+    """A remap between two seeded random layouts and back, every byte against
+    the oracle."""
+    import torch
+    dev = need_gpu()
+    name, ls, ld, ols, old, elem = _random_remap_cases(lego)[i]
+    n = ols.size()
+    src = {1: lambda: (S.int_tensor(n) % 251).to(torch.uint8), 2: lambda: S.tensor(n, "f16", seed=7),
+           4: lambda: S.tensor(n, "f32", seed=7), 8: lambda: S.int_tensor(n, bits=64)}[elem]()
+    say(f"remap {name} plan={lego.remap_plan(ls, ld, elem)['info']}")
+    out = _run(lego, ls, ld, src, dev)
+    exp = OR.remap(ols, old, bits(src))
+    assert (bits(out) == exp).all(), name
+    say(f"remap back {name} plan={lego.remap_plan(ld, ls, elem)['info']}")
+    back = _run(lego, ld, ls, out, dev)
+    assert (bits(back) == bits(src)).all(), name
+
+
 def _expand_cases(L):
     """ExpandBy (Section III-D, Figure 9): compact arrays whose extents the
     tiles do not divide, against tiled layouts of the padded shape."""
