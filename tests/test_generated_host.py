@@ -541,6 +541,22 @@ def test_index_sources_of_gpu_cases():
                     assert (got.reshape(-1, len(olay.dims())) == OL.inv_all(olay)).all(), name
 
 
+def test_index_sources_of_random_cases():
+    import paper_2505_08091_amd as L
+    from tests.test_gpu_index import _random_index_cases
+    with tempfile.TemporaryDirectory() as tmp:
+        out = os.path.join(tmp, "out.bin")
+        for name, lay, olay in _random_index_cases(L):
+            for kind in ("apply", "inv"):
+                src = L.plan_source(kind, lay, param=8)
+                _compile_and_run(src, HARNESS_INDEX, tmp, [out])
+                got = np.fromfile(out, dtype=np.int64)
+                if kind == "apply":
+                    assert (got == OL.apply_all(olay)).all(), name
+                else:
+                    assert (got.reshape(-1, len(olay.dims())) == OL.inv_all(olay)).all(), name
+
+
 def _remap_cases():
     import paper_2505_08091_amd as L
     from tests.test_gpu_genexpr import _expr_cases
@@ -649,7 +665,7 @@ def _gemm_cases():
     return cases
 
 
-N_GEMM_CASES = 70
+N_GEMM_CASES = 82
 
 
 def test_gemm_case_count():

@@ -366,7 +366,7 @@ def test_gemm_ragged_sizes(lego, i):
 
 
 def _random_cases(L):
-    """24 GEMM configurations drawn from a fixed seed: fp16 or bf16; A
+    """36 GEMM configurations drawn from fixed seeds: fp16 or bf16; A
     row-major, column-major or in Morton order (power-of-two M and K), B row-
     or column-major; the default tiles or one of six smaller tile and wave
     shapes; ragged sizes unless A is in Morton order; and now and then a
@@ -404,10 +404,40 @@ def _random_cases(L):
         if rng.integers(3) == 0:
             kw["max_workgroups"] = int(rng.integers(1, 8))
         out.append(kw)
+    # 12 more with explicit tiles, LDS layouts given as XOR swizzles of random
+    # granule and stride, and a workgroup order given as a layout
+    rng = np.random.default_rng(2506)
+    while len(out) < 36:
+        dt = ("f16", "bf16")[rng.integers(2)]
+        la, lb = ("Row", "Col")[rng.integers(2)], ("Row", "Col")[rng.integers(2)]
+        t = tiles[1 + rng.integers(len(tiles) - 1)]
+        bm, bn, bk = t[0], t[1], t[2]
+        M, N, K = bm * int(rng.integers(1, 4)), bn * int(rng.integers(1, 4)), bk * int(rng.integers(1, 5))
+        kw = dict(M=M, N=N, K=K, dtype=dt, bm=bm, bn=bn, bk=bk, wm=t[3], wn=t[4])
+        kw["a"], kw["oa"] = L.as_layout(getattr(L, la)(M, K)), OL.as_layout(getattr(OL, la)(M, K))
+        kw["b"], kw["ob"] = L.as_layout(getattr(L, lb)(K, N)), OL.as_layout(getattr(OL, lb)(K, N))
+        for side, rows in (("lds_a", bm), ("lds_b", bn)):
+            if rng.integers(2):
+                v = int((8, 16, 32)[rng.integers(3)])
+                if v <= bk:
+                    kw[side] = L.as_layout(L.GenP("xor_swizzle", [rows, bk], [v, int(rng.integers(1, 5))]))
+        mt, nt = M // bm, N // bn
+        sched = rng.integers(4)
+        if sched == 1:
+            kw["sched"] = L.as_layout(L.Col(mt, nt))
+        elif sched == 2:
+            kw["sched"] = L.as_layout(L.GenP("reverse", [mt, nt]))
+        elif sched == 3 and mt & (mt - 1) == 0 and nt & (nt - 1) == 0:
+            kw["sched"] = L.as_layout(L.GenP("morton", [mt, nt]))
+        try:
+            L.gemm_plan(M, N, K, dt, **{k: v for k, v in kw.items() if k not in ("M", "N", "K", "dtype", "oa", "ob")})
+        except L.LegoError:
+            continue
+        out.append(kw)
     return out
 
 
-@pytest.mark.parametrize("i", range(24))
+@pytest.mark.parametrize("i", range(36))
 def test_gemm_random_configs(lego, i):
     """Every output element of a seeded random GEMM configuration against the
     fp64 oracle (C pre-filled with NaN)."""

@@ -60,6 +60,34 @@ def test_index_maps_small(lego, idx_bytes):
         assert (inv.cpu().numpy() == OL.inv_all(olay)).all(), name
 
 
+def _random_index_cases(L):
+    """48 seeded random layouts: both sides of the random remap cases (one to
+    three tile levels, each a row/column-major, reversed, XOR-swizzled, Morton
+    or antidiagonal piece)."""
+    from tests.test_gpu_remap import _random_remap_cases
+    out = []
+    for name, ls, ld, ols, old, _ in _random_remap_cases(L):
+        out += [(name + " src", ls, ols), (name + " dst", ld, old)]
+    return out
+
+
+@pytest.mark.parametrize("idx_bytes", [4, 8])
+def test_index_maps_random(lego, idx_bytes):
+    import torch
+    dev = need_gpu()
+    dt = torch.int32 if idx_bytes == 4 else torch.int64
+    for name, lay, olay in _random_index_cases(lego):
+        n = olay.size()
+        say(f"apply_all/inv_all {name} n={n} idx_bytes={idx_bytes}")
+        out = torch.full((n,), -7, dtype=dt, device=dev)
+        lego.apply_all_device(lay, out)
+        inv = torch.full((n, len(olay.dims())), -7, dtype=dt, device=dev)
+        lego.inv_all_device(lay, inv)
+        torch.cuda.synchronize()
+        assert (out.cpu().numpy() == OL.apply_all(olay)).all(), name
+        assert (inv.cpu().numpy() == OL.inv_all(olay)).all(), name
+
+
 def test_index_map_c2_full_size(lego):
     """The 8192^2 blocked layout on all 2^26 points (bit-exact)."""
     import torch
