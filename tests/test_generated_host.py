@@ -541,6 +541,23 @@ def test_index_sources_of_gpu_cases():
                     assert (got.reshape(-1, len(olay.dims())) == OL.inv_all(olay)).all(), name
 
 
+@pytest.mark.parametrize("i", range(20))
+def test_remap_sources_of_random_expand_and_box_cases(i):
+    """The seeded random ExpandBy and antidiagonal remaps of the GPU tests,
+    both directions, on the host (padding reads -1 here: zero fill)."""
+    import paper_2505_08091_amd as L
+    from tests.test_gpu_remap import _random_box_cases, _random_expand_cases
+    name, ls, ld, ols, old, elem = (_random_expand_cases(L) + _random_box_cases(L))[i]
+    with tempfile.TemporaryDirectory() as tmp:
+        out = os.path.join(tmp, "out.bin")
+        for a, b, oa, ob in ((ls, ld, ols, old), (ld, ls, old, ols)):
+            src = L.plan_source("remap", a, b, param=elem)
+            _compile_and_run(src, HARNESS_REMAP, tmp, [out])
+            perm = np.fromfile(out, dtype=np.int64)
+            exp = OR.remap(oa, ob, np.arange(1, OR.phys_size(oa) + 1, dtype=np.int64)) - 1
+            assert (perm == exp).all(), name
+
+
 def test_index_sources_of_random_cases():
     import paper_2505_08091_amd as L
     from tests.test_gpu_index import _random_index_cases

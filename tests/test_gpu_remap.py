@@ -290,6 +290,89 @@ def test_remap_random_layouts(lego, i):
     assert (bits(back) == bits(src)).all(), name
 
 
+def _random_expand_cases(L):
+    """12 seeded ExpandBy remaps: a compact row- or column-major array of
+    ragged 2-D or 3-D extents against a random tiled layout of the padded
+    shape (tiles of 1 to 16 per axis, each level a random piece in 2-D)."""
+    rng = np.random.default_rng(91)
+    out = []
+    while len(out) < 12:
+        d = 2 if rng.integers(3) else 3
+        tile = [int((1, 2, 3, 4, 5, 8, 16)[rng.integers(7)]) for _ in range(d)]
+        n = [int(rng.integers(1, 90 if d == 2 else 30)) for _ in range(d)]
+        ne = [-(-a // t) * t for a, t in zip(n, tile)]
+        if ne == n:
+            continue
+        inner = ("Row", "Col")[rng.integers(2)]
+        ls = L.ExpandBy(n, ne, L.as_layout(getattr(L, inner)(*ne)))
+        ols = OL.ExpandBy(n, ne, OL.as_layout(getattr(OL, inner)(*ne)))
+        if d == 2:
+            ld, old = _random_layout(L, rng, ne[0], ne[1], [tuple(tile)])
+        else:
+            outer = [a // t for a, t in zip(ne, tile)]
+            ld, old = L.TileOrderBy(L.Row(*outer), L.Row(*tile)), OL.TileOrderBy(OL.Row(*outer), OL.Row(*tile))
+        elem = int((1, 2, 4, 8)[rng.integers(4)])
+        out.append((f"expand {n} into {ne} tiles {tile} {elem} B", ls, ld, ols, old, elem))
+    return out
+
+
+def _random_box_cases(L):
+    """8 seeded remaps between a whole matrix in antidiagonal order (Figure 7)
+    and a row-major, column-major or tiled layout, at sizes from 64 to 700
+    (the box path, ragged last boxes included)."""
+    rng = np.random.default_rng(92)
+    out = []
+    while len(out) < 8:
+        n = int(rng.integers(64, 700))
+        tiles = [] if rng.integers(2) else [(t, t) for t in (1, 2, 4, 5, 7, 8) if n % t == 0][-1:]
+        ls, ols = _random_layout(L, rng, n, n, tiles) if tiles else (
+            (L.as_layout(L.Row(n, n)), OL.as_layout(OL.Row(n, n))) if rng.integers(2) else
+            (L.as_layout(L.Col(n, n)), OL.as_layout(OL.Col(n, n))))
+        ld, old = L.as_layout(L.GenP("antidiag", [n, n])), OL.as_layout(OL.antidiag_genp(n))
+        elem = int((1, 2, 4, 8)[rng.integers(4)])
+        out.append((f"antidiagonal {n}^2 tiles {tiles} {elem} B", ls, ld, ols, old, elem))
+    return out
+
+
+def _fill(n, elem):
+    import torch
+    return {1: lambda: (S.int_tensor(n) % 251).to(torch.uint8), 2: lambda: S.tensor(n, "f16", seed=7),
+            4: lambda: S.tensor(n, "f32", seed=7), 8: lambda: S.int_tensor(n, bits=64)}[elem]()
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_remap_random_expandby(lego, i):
+    """Pad a compact array into a random tiled layout (padding must read
+    back zero) and crop it back, every byte against the oracle."""
+    import torch
+    dev = need_gpu()
+    name, ls, ld, ols, old, elem = _random_expand_cases(lego)[i]
+    src = _fill(OR.phys_size(ols), elem)
+    say(f"remap {name} plan={lego.remap_plan(ls, ld, elem)['info']}")
+    d_pad = torch.full((OR.phys_size(old),), 1, dtype=src.dtype, device=dev)
+    lego.remap(ls, ld, src.to(dev), d_pad)
+    torch.cuda.synchronize()
+    assert (bits(d_pad.cpu()) == OR.remap(ols, old, bits(src))).all(), name
+    say(f"remap crop {name} plan={lego.remap_plan(ld, ls, elem)['info']}")
+    d_back = torch.empty(src.numel(), dtype=src.dtype, device=dev)
+    lego.remap(ld, ls, d_pad, d_back)
+    torch.cuda.synchronize()
+    assert (bits(d_back.cpu()) == bits(src)).all(), name
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_remap_random_antidiagonal(lego, i):
+    dev = need_gpu()
+    name, ls, ld, ols, old, elem = _random_box_cases(lego)[i]
+    src = _fill(ols.size(), elem)
+    say(f"remap {name} plan={lego.remap_plan(ls, ld, elem)['info']}")
+    out = _run(lego, ls, ld, src, dev)
+    assert (bits(out) == OR.remap(ols, old, bits(src))).all(), name
+    say(f"remap back {name} plan={lego.remap_plan(ld, ls, elem)['info']}")
+    back = _run(lego, ld, ls, out, dev)
+    assert (bits(back) == bits(src)).all(), name
+
+
 def _expand_cases(L):
     """ExpandBy (Section III-D, Figure 9): compact arrays whose extents the
     tiles do not divide, against tiled layouts of the padded shape."""
