@@ -679,10 +679,13 @@ def _gemm_cases():
     cases += [{k: v for k, v in _morton_direct_kw(L, c).items() if k != "max_workgroups"} for c in _morton_direct_cases(L)]
     from tests.test_gpu_gemm import _random_cases
     cases += [{k: v for k, v in c.items() if k not in ("oa", "ob", "max_workgroups")} for c in _random_cases(L)]
+    M, N, K = 32768, 256, 32768  # a 2 GiB operand
+    cases.append(dict(M=M, N=N, K=K, dtype="bf16", a=L.as_layout(L.Row(M, K)), b=L.as_layout(L.Col(K, N))))
+    cases.append(dict(M=M, N=N, K=K, dtype="bf16", a=L.as_layout(L.Col(M, K)), b=L.as_layout(L.Row(K, N))))
     return cases
 
 
-N_GEMM_CASES = 82
+N_GEMM_CASES = 84
 
 
 def test_gemm_case_count():

@@ -460,6 +460,43 @@ def test_gemm_random_configs(lego, i):
     assert ok, (mre, fre)
 
 
+@pytest.mark.parametrize("layouts", ["row_col", "col_row"])
+def test_gemm_operand_of_2gib(lego, layouts):
+    """A 32768 x 32768 bf16 A operand (2 GiB: copies through 64-bit
+    addresses, not the range-checked buffer loads), N = 256: two sampled rows
+    of every 256-row tile row against the fp64 oracle.  The operands are made
+    on the device by a seeded torch generator and the sampled rows read
+    back as inputs of the check."""
+    import torch
+    dev = need_gpu()
+    M, N, K = 32768, 256, 32768
+    la, lb = ("Row", "Col") if layouts == "row_col" else ("Col", "Row")
+    kw = dict(a=lego.as_layout(getattr(lego, la)(M, K)), b=lego.as_layout(getattr(lego, lb)(K, N)))
+    plan = lego.gemm_plan(M, N, K, "bf16", **kw)
+    say(f"gemm 2 GiB operand {layouts} plan={plan}")
+    g = torch.Generator(device=dev)
+    g.manual_seed(2505)
+    a = torch.randn(M * K, generator=g, device=dev).to(torch.bfloat16)
+    b = torch.randn(K * N, generator=g, device=dev).to(torch.bfloat16)
+    c = torch.full((M * N,), float("nan"), dtype=torch.float32, device=dev)
+    lego.gemm(a, b, c, M, N, K, "bf16", **kw)
+    torch.cuda.synchronize()
+    rows = np.sort(np.concatenate([np.arange(0, M, 256), np.arange(0, M, 256) + 255 - np.arange(M // 256) % 256]))
+    ri = torch.from_numpy(rows).to(dev)
+    if la == "Row":
+        a_rows = a.view(M, K)[ri]
+    else:
+        a_rows = a.view(K, M)[:, ri].t().contiguous()
+    a_bits = a_rows.view(torch.int16).cpu().numpy().view(np.uint16)  # the sampled rows, row-major
+    b_bits = b.view(torch.int16).cpu().numpy().view(np.uint16)
+    r = OG.gemm(a_bits, b_bits, OL.as_layout(OL.Row(rows.size, K)), OL.as_layout(getattr(OL, lb)(K, N)), "bf16")
+    got = c.view(M, N)[ri].cpu().numpy()
+    assert np.isfinite(got).all()
+    ok, mre, fre = OG.check_tolerance(got, r)
+    assert ok, (mre, fre)
+    del a, b, c
+
+
 def _persistent_cases(L):
     """GEMMs whose workgroups each walk several output tiles (the plan is
     persistent and max_workgroups is below the tile count), so the LDS ring
