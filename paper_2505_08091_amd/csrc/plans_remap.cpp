@@ -496,8 +496,14 @@ static RemapPlan plan_remap_impl(const Layout& src, const Layout& dst, int elem_
   // previous remap's output; cached stores leave that output in the last-level
   // cache for its consumer.  An element gather reads each source line many
   // times over neighbouring chunks, so its loads stay cached (Row <->
-  // antidiagonal 4096^2 fp32: 0.74/0.97 -> 1.11/1.78 TB/s).
+  // antidiagonal 4096^2 fp32: 0.74/0.97 -> 1.11/1.78 TB/s).  An LDS-staged
+  // remap of at most 32 MiB per buffer streams its stores too: written
+  // through the L2 of each XCD, the output of a launch this small slowed
+  // the next launch that read it (2048^2 fp32 transposes alternating: 2.76 /
+  // 4.42 -> 4.02 / 3.94 TB/s; Row <-> Morton 4096^2 fp16 after a cache
+  // flush 4.43 / 4.73 -> 4.92 / 4.90, hot unchanged overall).
   int nontemporal = R.path == REMAP_GATHER ? 0 : 1;
+  if (R.path == REMAP_LDS && N * elem_bytes <= (i64(32) << 20)) nontemporal = 3;
   nontemporal = (int)tune("remap.nontemporal", nontemporal);
   if (R.path == REMAP_DIRECT || R.path == REMAP_GATHER) {
     // 8 vectors in flight per thread (a 32 KiB chunk per workgroup at 16-byte
