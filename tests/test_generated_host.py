@@ -584,7 +584,39 @@ def _remap_cases():
                       OL.as_layout(OL.Row(n, n)), OL.as_layout(OL.Col(n, n))))
     cases.append(("identity 8192", L.as_layout(L.Row(8192, 8192)), L.as_layout(L.Row(8192, 8192)),
                   OL.as_layout(OL.Row(8192, 8192)), OL.as_layout(OL.Row(8192, 8192))))
+    from tests.test_gpu_genexpr import _wavefront
+    cases.append(("wavefront 8192", L.as_layout(L.Row(8192, 8192)), _wavefront(L, None, 8192, 64),
+                  OL.as_layout(OL.Row(8192, 8192)), _wavefront(None, OL, 8192, 64)))
+    n, ne = 8000, 8192
+    cases.append(("pad 8000 into 8192 blocked", L.ExpandBy([n, n], [ne, ne], L.as_layout(L.Row(ne, ne))),
+                  L.TileOrderBy(L.Col(ne // 64, ne // 64), L.Row(64, 64)),
+                  OL.ExpandBy([n, n], [ne, ne], OL.as_layout(OL.Row(ne, ne))),
+                  OL.TileOrderBy(OL.Col(ne // 64, ne // 64), OL.Row(64, 64))))
     return cases
+
+
+def _check_remap_sources(L, ls, ld, ols, old, elem_bytes, tmp, name):
+    out = os.path.join(tmp, "out.bin")
+    for a, b, oa, ob in ((ls, ld, ols, old), (ld, ls, old, ols)):
+        src = L.plan_source("remap", a, b, param=elem_bytes)
+        _compile_and_run(src, HARNESS_REMAP, tmp, [out])
+        perm = np.fromfile(out, dtype=np.int64)
+        # source element k is tagged k + 1, so zero fill reads as -1
+        exp = OR.remap(oa, ob, np.arange(1, OR.phys_size(oa) + 1, dtype=np.int64)) - 1
+        assert (perm == exp).all(), (name, elem_bytes)
+
+
+_BIG = 1 << 23  # cases above this many elements run once each (4-byte elements), in parallel
+
+
+@pytest.mark.parametrize("i", range(5))
+def test_remap_sources_of_big_gpu_cases(i):
+    import paper_2505_08091_amd as L
+    big = [c for c in _remap_cases() if OL.prod(c[3].dims()) > _BIG]
+    assert len(big) == 5
+    name, ls, ld, ols, old = big[i]
+    with tempfile.TemporaryDirectory() as tmp:
+        _check_remap_sources(L, ls, ld, ols, old, 4, tmp, name)
 
 
 @pytest.mark.parametrize("elem_bytes", [1, 2, 4, 8])
@@ -593,7 +625,7 @@ def test_remap_sources_of_gpu_cases(elem_bytes):
     with tempfile.TemporaryDirectory() as tmp:
         out = os.path.join(tmp, "out.bin")
         for name, ls, ld, ols, old in _remap_cases():
-            if OL.prod(ols.dims()) > (1 << 23) and elem_bytes != 4:
+            if OL.prod(ols.dims()) > _BIG:
                 continue
             for a, b, oa, ob in ((ls, ld, ols, old), (ld, ls, old, ols)):
                 src = L.plan_source("remap", a, b, param=elem_bytes)

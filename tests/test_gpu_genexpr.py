@@ -26,6 +26,29 @@ def _wavefront(L, G, n, t):
         L.GenPExpr([q, q], GE.ANTIDIAG_APPLY, GE.ANTIDIAG_INV), L.Row(t, t))
 
 
+def test_remap_wavefront_8192_full(lego):
+    """The measured size: 8192^2 fp32 into 64 x 64 tiles in wavefront order
+    (the expression GenP over the 128 x 128 tile grid) and back, every element
+    against the oracle."""
+    import torch
+    dev = need_gpu()
+    n = 8192
+    ls, ld = lego.as_layout(lego.Row(n, n)), _wavefront(lego, None, n, 64)
+    ols, old = OL.as_layout(OL.Row(n, n)), _wavefront(None, OL, n, 64)
+    src = S.tensor(n * n, "f32", seed=S.SEED_SRC)
+    say(f"remap wavefront 8192^2 plan={lego.remap_plan(ls, ld, 4)['info']}")
+    d_src = src.to(dev)
+    d_w = torch.empty_like(d_src)
+    lego.remap(ls, ld, d_src, d_w)
+    torch.cuda.synchronize()
+    assert (d_w.cpu().numpy().view(np.uint32) == OR.remap(ols, old, src.numpy().view(np.uint32))).all()
+    say(f"remap wavefront 8192^2 back plan={lego.remap_plan(ld, ls, 4)['info']}")
+    d_back = torch.empty_like(d_src)
+    lego.remap(ld, ls, d_w, d_back)
+    torch.cuda.synchronize()
+    assert torch.equal(d_back.cpu(), src)
+
+
 SKEW_APPLY = "i1 * n0 + (i0 + i1) % n0"
 SKEW_INV = ["(x % n0 + n0 - (x / n0) % n0) % n0", "x / n0"]
 

@@ -392,6 +392,30 @@ def _expand_cases(L):
     return out
 
 
+def test_remap_pad_crop_8000_in_8192_full(lego):
+    """The measured size: an 8000 x 8000 fp32 array into a zero-padded
+    8192 x 8192 blocked buffer (64 x 64 tiles, column-major tile order) and
+    back, every element against the oracle (padding must read back zero)."""
+    import torch
+    dev = need_gpu()
+    n, ne = 8000, 8192
+    ls = lego.ExpandBy([n, n], [ne, ne], lego.as_layout(lego.Row(ne, ne)))
+    ld = lego.TileOrderBy(lego.Col(ne // 64, ne // 64), lego.Row(64, 64))
+    ols = OL.ExpandBy([n, n], [ne, ne], OL.as_layout(OL.Row(ne, ne)))
+    old = OL.TileOrderBy(OL.Col(ne // 64, ne // 64), OL.Row(64, 64))
+    src = S.tensor(n * n, "f32", seed=S.SEED_SRC)
+    say(f"remap pad 8000^2 into 8192^2 blocked plan={lego.remap_plan(ls, ld, 4)['info']}")
+    d_pad = torch.full((ne * ne,), 1.0, dtype=torch.float32, device=dev)
+    lego.remap(ls, ld, src.to(dev), d_pad)
+    torch.cuda.synchronize()
+    assert (bits(d_pad.cpu()) == OR.remap(ols, old, bits(src))).all()
+    say(f"remap crop 8192^2 blocked to 8000^2 plan={lego.remap_plan(ld, ls, 4)['info']}")
+    d_back = torch.empty(n * n, dtype=torch.float32, device=dev)
+    lego.remap(ld, ls, d_pad, d_back)
+    torch.cuda.synchronize()
+    assert torch.equal(d_back.cpu(), src)
+
+
 @pytest.mark.parametrize("elem", ["f32", "f16", "i64", "u8"])
 def test_remap_expandby_pad_and_crop(lego, elem):
     """Compact -> padded tiled buffer (zero padding) -> compact again."""
