@@ -289,6 +289,38 @@ def test_gemm_operand_layouts_4096(lego, la_name, lb_name):
     assert ok, (mre, fre)
 
 
+@pytest.mark.parametrize("la_name,lb_name", [("Row", "Row"), ("Row", "Col"), ("Col", "Row"), ("Col", "Col")])
+def test_gemm_operand_layouts_8192(lego, la_name, lb_name):
+    """The four Row/Col operand variants at the measured 8192^3 fp16, default
+    plan: every output element against the fp64 oracle."""
+    M = N = K = 8192
+    a = S.tensor(M * K, "f16", seed=S.SEED_A)
+    b = S.tensor(K * N, "f16", seed=S.SEED_B)
+    kw = dict(a=lego.as_layout(getattr(lego, la_name)(M, K)), b=lego.as_layout(getattr(lego, lb_name)(K, N)))
+    say(f"gemm 8192 A {la_name} B {lb_name} plan={lego.gemm_plan(M, N, K, 'f16', **kw)}")
+    c = _run(lego, a, b, M, N, K, "f16", **kw).reshape(M, N)
+    assert np.isfinite(c).all()
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(getattr(OL, la_name)(M, K)),
+                OL.as_layout(getattr(OL, lb_name)(K, N)), "f16")
+    ok, mre, fre = OG.check_tolerance(c, r)
+    assert ok, (mre, fre)
+
+
+def test_gemm_ragged_8000_bf16_full(lego):
+    """The measured partial-tile GEMM, 8000^3 bf16 with 256-wide tiles that
+    overhang the matrices: every output element against the fp64 oracle."""
+    M = N = K = 8000
+    a = S.tensor(M * K, "bf16", dist="normal", seed=S.SEED_A)
+    b = S.tensor(K * N, "bf16", dist="normal", seed=S.SEED_B)
+    say(f"gemm ragged 8000^3 plan={lego.gemm_plan(M, N, K, 'bf16')}")
+    c = _run(lego, a, b, M, N, K, "bf16").reshape(M, N)
+    assert np.isfinite(c).all()
+    r = OG.gemm(S.as_numpy_bits(a), S.as_numpy_bits(b), OL.as_layout(OL.Row(M, K)), OL.as_layout(OL.Col(K, N)),
+                "bf16")
+    ok, mre, fre = OG.check_tolerance(c, r)
+    assert ok, (mre, fre)
+
+
 def test_gemm_errors(lego):
     import torch
     dev = need_gpu()
