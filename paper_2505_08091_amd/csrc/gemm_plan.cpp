@@ -893,8 +893,20 @@ GemmPlan plan_gemm_waves(const GemmRequest& rq0, bool wide_waves) {
     opsinfo << " " << f.first << ":" << e.ops;
   }
 
+  // MFMA blocks of a wave tile with a row (column) inside C in some tile:
+  // the first row of block i (column of block j) in the first wave of the
+  // first tile is its least, so the blocks with no element in range in any
+  // tile are a suffix (M or N below one tile).  Row pairs are read together.
+  int mi_live = 0, ni_live = 0;
+  for (int i = 0; i < MI; ++i)
+    if ((ops[0].mpair ? (i / 2) * 2 * MB + i % 2 : i * MB) < M) mi_live = i + 1;
+  if (ops[0].mpair && mi_live % 2) ++mi_live;
+  for (int j = 0; j < NI; ++j)
+    if (j * MB < N) ni_live = j + 1;
+
   std::ostringstream s;
   s << prelude_text() << "#define IDX_T " << (wide ? "i64" : "u32") << "\n"
+    << "#define MI_LIVE " << mi_live << "\n#define NI_LIVE " << ni_live << "\n"
     << "#define BM " << bm << "\n#define BN " << bn << "\n#define BK " << bk << "\n#define MB " << MB
     << "\n#define KB " << KB << "\n#define MI " << MI << "\n#define NI " << NI << "\n#define NWAVES " << NWAVES
     << "\n#define NT " << NT << "\n#define KT " << Kt << "u\n#define IN_BF16 " << (rq.dtype == LEGO_BF16 ? 1 : 0)

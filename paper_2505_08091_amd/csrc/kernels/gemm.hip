@@ -9,6 +9,8 @@
 //   BM BN BK         workgroup tile
 //   MB KB            MFMA block (32x32x16 or 16x16x32)
 //   MI NI            MFMA blocks per wave along m and n
+//   MI_LIVE NI_LIVE  the leading blocks of these that hold some element of C
+//                    (fewer only where M or N is below one tile)
 //   NWAVES NT KT     waves per workgroup, threads (64 * NWAVES), K / BK
 //   IN_BF16          1: bf16 inputs, 0: fp16
 //   A_NV A_V A_SEP A_SVEC A_FRVEC A_NVEC A_GUARD (and B_*): vectors per thread
@@ -92,18 +94,25 @@ LEGO_FN mf_t lds_frag_dw(const elem_t* base, IDX_T o0, IDX_T o1, IDX_T o2, IDX_T
 }
 
 // Fragment through two transposing LDS loads (ds_read_b64_tr_b16): elements
-// 0-3 from the addresses of half 0, elements 4-7 from those of half 1.  The
-// loads are issued as inline assembly: the compiler's own form of this load is
-// ordered behind every direct global-to-LDS copy in flight (a full vmcnt wait
-// before each read), which would serialize the copies with the MFMAs.  The
-// compiler does not track these loads, so FRAG_WAIT below waits for them
-// before their fragments are used and before every barrier.
+// 0-3 from the addresses of half 0, elements 4-7 from those of half 1.  With
+// direct global-to-LDS copies the loads are issued as inline assembly: the
+// compiler's own form of this load is ordered behind every direct copy in
+// flight (a full vmcnt wait before each read), which would serialize the
+// copies with the MFMAs.  The compiler does not track these loads, so
+// FRAG_WAIT below waits for them before their fragments are used and before
+// every barrier.  Register-staged plans have no such copies and use the
+// compiler's form.
 typedef short s4_t __attribute__((ext_vector_type(4)));
 LEGO_FN s4_t lds_read_tr(const elem_t* p) {
+#if DIRECT_LDS
   s4_t r;
   const unsigned a = (unsigned)(unsigned long)(__attribute__((address_space(3))) const void*)p;
   asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(a));
   return r;
+#else
+  // No global-to-LDS copies in flight: the compiler's own (tracked) form.
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4_t*)p);
+#endif
 }
 LEGO_FN mf_t lds_frag_tr(const elem_t* base, IDX_T off0, IDX_T off1) {
   const s4_t lo = lds_read_tr(base + off0);
@@ -163,7 +172,7 @@ static_assert(FRAG_DIST == 1 || (FRAG_DIST < BK / KB && NFB > FRAG_DIST), "fragm
 // LDS read instructions per fragment.
 #define A_FRD (A_FRTR ? 2 : (A_FRVEC || A_FRZP ? 1 : (A_FRDW ? 2 : 8)))
 #define B_FRD (B_FRTR ? 2 : (B_FRVEC ? 1 : (B_FRDW ? 2 : 8)))
-#define FRAG_READS (MI * A_FRD + NI * B_FRD)
+#define FRAG_READS (MI_LIVE * A_FRD + NI_LIVE * B_FRD)
 
 template <bool B>
 struct lego_bool {
@@ -215,8 +224,19 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   // operand-swapped MFMAs write 32-byte pieces of 32 rows and measured 20%
   // slower on the 8192^3 bf16 GEMM.
   auto store_c = [&](IDX_T tm_, IDX_T tn_) {
+    // The tile's offset is opaque to the compiler: with one tile it is a
+    // constant, and the compiler then built all 256 store addresses of a
+    // lane ahead of the k-loop (512 VGPRs) and spilled them.  (An integer, so
+    // that C keeps its global address space and the stores stay global
+    // stores, which do not count against the LDS wait counter.)
 #if C_SEP
-    float* __restrict__ Cb = C + c_t(tm_, tn_);
+    IDX_T ct = c_t(tm_, tn_);
+    asm volatile("" : "+v"(ct));
+    float* __restrict__ Cb = C + ct;
+#else
+    IDX_T ct = 0;
+    asm volatile("" : "+v"(ct));
+    float* __restrict__ Cb = C + ct;
 #endif
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -230,7 +250,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #if C_SEP
           __builtin_nontemporal_store(acc[i][j][r], Cb + c_l(lane, w, i, j, r));
 #else
-          __builtin_nontemporal_store(acc[i][j][r], C + c_f(tm_, tn_, lane, w, i, j, r));
+          __builtin_nontemporal_store(acc[i][j][r], Cb + c_f(tm_, tn_, lane, w, i, j, r));
 #endif
         }
   };
@@ -328,7 +348,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
   auto fload_part = [&](const elem_t* la, const elem_t* lb, int s, int buf, int lo, int hi) {
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
-      if (i < lo || i >= hi) continue;
+      if (i < lo || i >= hi || i >= MI_LIVE) continue;
 #if A_FRTR
       af[buf][i] = lds_frag_tr(la, a_ft(lane, w, i, s, 0), a_ft(lane, w, i, s, 1));
 #elif A_FRVEC
@@ -359,7 +379,7 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     }
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
-      if (MI + j < lo || MI + j >= hi) continue;
+      if (MI + j < lo || MI + j >= hi || j >= NI_LIVE) continue;
 #if B_FRTR
       bf[buf][j] = lds_frag_tr(lb, b_ft(lane, w, j, s, 0), b_ft(lane, w, j, s, 1));
 #elif B_FRVEC
@@ -399,10 +419,14 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
     return af[fb][r];
 #endif
   };
+  // Blocks past MI_LIVE / NI_LIVE hold no element of C in any tile: they
+  // are neither read nor multiplied (their dead reads could otherwise share
+  // registers with live values while in flight).
   auto mfma_row = [&](int r, int fb) {
+    if (r >= MI_LIVE) return;
     const mf_t a = a_op(r, fb);
 #pragma unroll
-    for (int j = 0; j < NI; ++j) acc[r][j] = MFMA(a, bf[fb][j], acc[r][j]);
+    for (int j = 0; j < NI_LIVE; ++j) acc[r][j] = MFMA(a, bf[fb][j], acc[r][j]);
   };
   auto mfma_all = [&](int fb) {
 #pragma unroll
@@ -703,24 +727,48 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
       // each step's stage is a constant and its fragment addresses are
       // loop-invariant registers (1.6% on the 8192^3 bf16 GEMM; plans with
       // two waves per SIMD lack the registers for them).
-      for (IDX_T kt = 0; kt < kt_end; kt += NSTAGES) {
+      // (a do-while: the compiler must see that a tile runs at least one
+      // step, or on the path without steps it would reuse the registers of
+      // fragment reads still in flight)
+      IDX_T kt = 0;
+      do {
 #pragma unroll
         for (int p = 0; p < NSTAGES; ++p) {
           const bool own = kt + p + NSTAGES < KT;
           kstep(p, own ? cur : nxt, (kt + p + NSTAGES) % KT);
         }
-      }
+        kt += NSTAGES;
+      } while (kt < kt_end);
     } else {
-      for (IDX_T kt = 0; kt < kt_end; ++kt) {
+      IDX_T kt = 0;
+      do {
         const bool own = kt + NSTAGES < KT;
         kstep((int)((stage0 + kt) % NSTAGES), own ? cur : nxt, (kt + NSTAGES) % KT);
-      }
+        ++kt;
+      } while (kt < kt_end);
     }
     // After the workgroup's last tile the fragment reads issued by the last
     // step are dead, and the epilogue may reuse their registers: wait for
     // them first (between tiles they hold the next tile's fragments, which
     // stay live across the epilogue).
-    if (!has_next) FRAG_WAIT();
+    if (!has_next) {
+      FRAG_WAIT();
+#if A_FRTR || B_FRTR
+      // The trailing reads (substeps 0 .. FRAG_DIST-1 of a step that does
+      // not exist) are dead to the compiler, which would hand their
+      // registers to the epilogue as soon as the reads are issued: using
+      // them here, after the wait, keeps them allocated until it.
+#pragma unroll
+      for (int t = 0; t < FRAG_DIST; ++t) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+          if (A_FRTR) asm volatile("" ::"v"(af[t % NFB][i]));
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+          if (B_FRTR) asm volatile("" ::"v"(bf[t % NFB][j]));
+      }
+#endif
+    }
     store_c(cur.tm, cur.tn);
     if (!has_next) break;
 #pragma unroll
