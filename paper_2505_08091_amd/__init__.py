@@ -21,6 +21,15 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIBPATH = os.path.join(_HERE, "liblego.so")
 if not os.path.exists(_LIBPATH):
     raise ImportError(f"{_LIBPATH} is missing: build it with __graft_entry__.build()")
+# The library must bind to the HIP runtime that torch loads.  Loaded first,
+# it would bring in the system's HIP and HSA runtimes and torch would then
+# load its own: two runtimes in one process, and the second one to open the
+# GPU finds no device.  torch loaded first provides the runtime's soname,
+# which the library's dependency then resolves to.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
 _lib = ctypes.CDLL(_LIBPATH)
 
 c_i64p = ctypes.POINTER(ctypes.c_int64)

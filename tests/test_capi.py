@@ -301,6 +301,23 @@ def test_jit_uses_installed_compiler(tmp_path):
         assert want in comment, (want, comment)
 
 
+def test_one_hip_runtime_whatever_the_import_order():
+    """Importing the package before torch leaves one HIP runtime and one HSA
+    runtime in the process (torch's): with two, the second to open the GPU
+    finds no device."""
+    import subprocess
+    import sys
+    code = ("import paper_2505_08091_amd\nimport torch\n"
+            "libs = {l.split()[-1] for l in open('/proc/self/maps') if 'amdhip64' in l or 'hsa-runtime64' in l}\n"
+            "print(len({os.path.basename(p).split('.so')[0] for p in libs}), len(libs))\n")
+    env = dict(os.environ, PYTHONPATH=ROOT)
+    r = subprocess.run([sys.executable, "-c", "import os\n" + code], capture_output=True, text=True, env=env,
+                       timeout=600)
+    assert r.returncode == 0, r.stderr[-2000:]
+    kinds, files = map(int, r.stdout.split())
+    assert kinds == files == 2, r.stdout
+
+
 def test_retain_release_reference_counts(lego):
     """A retained handle outlives one release; the library drops it with the
     last one (composition holds its own references)."""
