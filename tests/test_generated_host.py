@@ -717,7 +717,7 @@ def _gemm_cases():
     return cases
 
 
-N_GEMM_CASES = 84
+N_GEMM_CASES = 86
 
 
 def test_gemm_case_count():

@@ -375,10 +375,18 @@ def _ragged_cases(L):
         dict(M=1002, N=520, K=1000, dtype="f16", a=L.TileOrderBy(L.Row(501, 250), L.Row(2, 4)),
              b=L.TileOrderBy(L.Row(250, 65), L.Col(4, 8)),
              oa=OL.TileOrderBy(OL.Row(501, 250), OL.Row(2, 4)), ob=OL.TileOrderBy(OL.Row(250, 65), OL.Col(4, 8))),
+        # M or N below one wave tile: whole MFMA blocks hold no element of C,
+        # with transposing fragment reads of B (N = 56 of 128, A Morton) and
+        # of A (M = 40 of 128, column-major)
+        dict(M=512, N=56, K=512, dtype="bf16", a=L.as_layout(L.GenP("morton", [512, 512])),
+             b=L.as_layout(L.Row(512, 56)), bm=128, bn=256, bk=64, wm=64, wn=128,
+             oa=OL.as_layout(OL.morton_genp(512, 512)), ob=OL.as_layout(OL.Row(512, 56))),
+        dict(M=40, N=512, K=128, dtype="f16", a=L.as_layout(L.Col(40, 128)), b=L.as_layout(L.Col(128, 512)),
+             bm=256, bn=256, bk=64, wm=128, wn=128, oa=OL.as_layout(OL.Col(40, 128)), ob=OL.as_layout(OL.Col(128, 512))),
     ]
 
 
-@pytest.mark.parametrize("i", range(10))
+@pytest.mark.parametrize("i", range(12))
 def test_gemm_ragged_sizes(lego, i):
     """Every output element of a GEMM with partial tiles against the oracle;
     C is pre-filled with NaN so a dropped or misplaced store shows."""
