@@ -761,10 +761,10 @@ extern "C" __global__ __launch_bounds__(NT) void lego_gemm(const elem_t* __restr
 #pragma unroll
       for (int t = 0; t < FRAG_DIST; ++t) {
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+        for (int i = 0; i < MI_LIVE; ++i)
           if (A_FRTR) asm volatile("" ::"v"(af[t % NFB][i]));
 #pragma unroll
-        for (int j = 0; j < NI; ++j)
+        for (int j = 0; j < NI_LIVE; ++j)
           if (B_FRTR) asm volatile("" ::"v"(bf[t % NFB][j]));
       }
 #endif
